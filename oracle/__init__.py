@@ -1,0 +1,37 @@
+"""CPU oracle for the DynamicPTQ quantized linear layer.
+
+TEST INFRASTRUCTURE ONLY.  This package is the plain, slow, obviously-correct
+definition of what the HIP path computes.  Only the test suite, the smoke check
+in ``__graft_entry__`` and the ``cpu_baseline`` leg of ``bench.py`` may import
+or run it; the product library never does, and it shares no code, tables or
+constants with the HIP sources.
+
+Every floating-point step is written out in fp32 in a pinned order (the paper
+fixes no precision or summation order for the rotation; the readings chosen
+here are listed in the module docstrings).  Integer work (codes, packing,
+accumulators) is exact.
+
+Modules
+  hadamard  Sylvester / Paley Hadamard matrices and the block rotation x.B_h
+            (Section 2, Eq. 4 "rotation_activation" and Eq. 5 "rotation_equiv").
+  quant     per-token / per-channel symmetric quantizer and nibble packing
+            (Section 2, Eq. 1-3; Section 4.2 quantizer facts).
+  gemm      exact integer GEMM and the per-token x per-channel dequant epilogue
+            (Section 2, Y = X W^T).
+  policy    phase-aware activation bit policy (Eq. 21, Algorithm 1 step 2).
+"""
+
+from .hadamard import (sylvester, paley28, hadamard, split_had_size,
+                       rotate_rows)
+from .quant import (qmax_for_bits, quantize_rows, pack_int4, unpack_int4,
+                    rotate_quant_ref, prepare_weights_ref, dequant_rows)
+from .gemm import qlinear_acc_ref, qlinear_acc_entries, epilogue_ref, qlinear_ref
+from .policy import layer_policy_ref
+
+__all__ = [
+    "sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows",
+    "qmax_for_bits", "quantize_rows", "pack_int4", "unpack_int4",
+    "rotate_quant_ref", "prepare_weights_ref", "dequant_rows",
+    "qlinear_acc_ref", "qlinear_acc_entries", "epilogue_ref", "qlinear_ref",
+    "layer_policy_ref",
+]
