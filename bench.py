@@ -1,0 +1,226 @@
+"""Benchmark of the DynamicPTQ quantized linear layer on one MI355X.
+
+Workload (one "step"): the LLaMA-2-7B fused QKV projection, M = 2048 prefill
+tokens, K = 4096, N = 12288, Hadamard 4096, with synthetic seeded fp16
+activations (N(0,1) plus 4 outlier channels x50-x200) and N(0, 0.02) weights
+quantized to 4 bits per output channel.  The layer policy (Eq. 21) is looked
+up for a 32-layer model, and the step runs the layer as a non-sensitive layer
+(A4) and then as a sensitive layer (A8): per precision one rotate+quantize
+launch and one GEMM launch, all on one stream.  Inputs are resident in HBM
+before timing; the step cycles through enough copies of activations and
+weights (> 256 MiB) that the Infinity Cache cannot hold them.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--extended]
+
+Prints one JSON line.  value = total integer ops (2 M N K per GEMM) / time.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, T ops/s
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
+METRIC = "W4A4/W4A8 qlinear TOPS (rotate+quant+GEMM), % int8 MFMA peak; decode GB/s"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--copies", type=int, default=12,
+                   help="distinct activation/weight copies cycled per step")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=24,
+                   help="token rows of the workload the CPU oracle is timed on")
+    p.add_argument("--extended", action="store_true",
+                   help="also time the decode shapes and the 28 x 512 rotation")
+    return p.parse_args()
+
+
+def _events(torch, n):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def time_layer(torch, dptq, cfg, args):
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
+    rng = np.random.default_rng(cfg["seed"])
+    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
+    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
+    wp, ws = dptq.prepare_weights(w, h)
+    del w
+    R = max(1, args.copies)
+    xs = [x.clone() for _ in range(R)]
+    wps = [wp.clone() for _ in range(R)]
+    wss = [ws.clone() for _ in range(R)]
+    codes = {4: torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
+             8: torch.empty((M, K), dtype=torch.int8, device=dev)}
+    scales = torch.empty((M,), dtype=torch.float32, device=dev)
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+
+    n_layers = 32
+    def step(i, ev=None):
+        bits_all = dptq.layer_policy(n_layers)
+        seq = (bits_all[n_layers // 2], bits_all[0])     # a non-sensitive, a sensitive layer
+        r = i % R
+        k = 0
+        for bits in seq:
+            if ev is not None:
+                ev[k].record()
+            dptq.rotate_quant(xs[r], h, bits, codes[bits], scales)
+            if ev is not None:
+                ev[k + 1].record()
+            dptq.qlinear(codes[bits], scales, bits, wps[r], wss[r], y)
+            k += 2
+        if ev is not None:
+            ev[k].record()
+        return seq
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [_events(torch, 5) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        seq = step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    # per-kernel durations (events bracket each launch on its stream)
+    names = [f"rotate_quant_a{seq[0]}", f"gemm_a{seq[0]}", f"rotate_quant_a{seq[1]}",
+             f"gemm_a{seq[1]}"]
+    per = {n: 0.0 for n in names}
+    for ev in evs:
+        for k, n in enumerate(names):
+            per[n] += ev[k].elapsed_time(ev[k + 1])
+    per = {n: v / args.steps for n, v in per.items()}
+    return wall, per, seq
+
+
+def time_decode(torch, dptq, args):
+    """Weight-streaming GB/s on the LLaMA-3-8B down_proj decode shapes."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    K, N, h = 14336, 4096, 28 * 512
+    rng = np.random.default_rng(2)
+    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
+    wp, ws = dptq.prepare_weights(w, h)
+    del w
+    R = 12
+    wps = [wp.clone() for _ in range(R)]
+    out = {}
+    for M in (1, 4, 16):
+        x = torch.from_numpy(workloads.student_t(rng, M, K)).to(dev)
+        for bits in (4, 8):
+            codes, scales = dptq.rotate_quant(x, h, bits)
+            y = torch.empty((M, N), dtype=torch.float16, device=dev)
+            for i in range(5):
+                dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)
+            reps = 60
+            e0, e1 = _events(torch, 2)
+            e0.record()
+            for i in range(reps):
+                dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            nbytes = N * K // 2 + 4 * N + M * K * bits // 8 + 4 * M + 2 * M * N
+            out[f"decode_M{M}_a{bits}"] = {"us": round(us, 2),
+                                           "GB/s": round(nbytes / us / 1e3, 1)}
+            e0, e1 = _events(torch, 2)
+            e0.record()
+            for i in range(reps):
+                dptq.rotate_quant(x, h, bits, codes, scales)
+            e1.record()
+            torch.cuda.synchronize()
+            out[f"rotate_quant_M{M}_a{bits}_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+    return out
+
+
+def cpu_baseline(cfg, rows, seed=123):
+    """Time the CPU oracle on a bounded sample: `rows` token rows of the same
+    layer, both precisions (rotation + quantization + exact GEMM + epilogue)."""
+    import numpy as np
+    import workloads
+    from oracle import rotate_quant_ref, qlinear_ref
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
+    rng = np.random.default_rng(seed)
+    x = workloads.gauss_outliers(rng, rows, K)
+    wp = workloads.random_weight_bytes(rng, N, K)
+    ws = workloads.random_scales(rng, N)
+    t0 = time.perf_counter()
+    for bits in (4, 8):
+        c, s = rotate_quant_ref(x, h, bits)
+        qlinear_ref(c, s, bits, wp, ws)
+    dt = time.perf_counter() - t0
+    ops = 2 * (2.0 * rows * N * K)
+    return {"value": round(ops / dt / 1e12, 6), "unit": "TOPS", "cores": int(blas_threads),
+            "kind": "oracle",
+            "sample": f"{rows} of {M} token rows, A4 and A8, K={K}, N={N}, h={h}: "
+                      f"rotation, quantization, exact GEMM and epilogue; {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the quantized linear has no multi-GPU path in this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2606_12487_amd as dptq
+    import workloads
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dptq.lib()
+    cfg = workloads.CONFIGS["llama2_7b_qkv"]
+    M, K, N = cfg["M"], cfg["K"], cfg["N"]
+
+    wall, per, seq = time_layer(torch, dptq, cfg, args)
+    ops_gemm = 2.0 * M * N * K
+    ops_step = ops_gemm * len(seq)
+    value = ops_step * args.steps / wall / 1e12
+    ms_step = wall * 1e3 / args.steps
+
+    gemm_a4_ms = per[f"gemm_a{seq[0]}"]
+    achieved = ops_gemm / (gemm_a4_ms * 1e-3) / 1e12
+    k1_bytes = 2 * M * K + M * K * 4 // 8 + 4 * M
+    rec = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": "llama2-7b fused qkv qlinear, rotate+quant+GEMM at A4 then A8",
+                   "M": M, "K": K, "N": N, "had_size": cfg["h"], "bits": list(seq),
+                   "parallelism": "none"},
+        "roofline": {"bound": "mfma", "kernel": "qgemm_prefill<4>",
+                     "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
+                     "traffic": None},
+        "kernels_ms": {k: round(v, 4) for k, v in per.items()},
+        "rotate_quant_a4_GBs": round(k1_bytes / (per[f"rotate_quant_a{seq[0]}"] * 1e-3) / 1e9, 1),
+    }
+    if args.extended:
+        rec["decode"] = time_decode(torch, dptq, args)
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(cfg, args.cpu_rows)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

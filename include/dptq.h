@@ -1,0 +1,150 @@
+/*
+ * dptq.h - C ABI of the DynamicPTQ quantized linear layer for AMD MI355X (gfx950).
+ *
+ * The library computes the inference hot path of a W4A4 / W4A8 linear layer as
+ * described by DynamicPTQ (arXiv 2606.12487):
+ *
+ *   1. an online Hadamard rotation of the fp16 activations (Section 2, Eq. 4),
+ *   2. per-token symmetric quantization to 4 bits, or to 8 bits on the layers
+ *      the phase-aware policy marks sensitive (Section 4.2; Algorithm 1 step 2;
+ *      Eq. 21),
+ *   3. an exact integer GEMM against packed 4-bit per-output-channel weights
+ *      (Y = X W^T, Section 2; weights pre-rotated offline, Eq. 5), followed by
+ *      a per-token x per-channel dequant epilogue.
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer named "device" is GPU memory owned by the caller; the
+ *     library never allocates, frees or retains memory and keeps no state
+ *     between calls.
+ *   - GPU work is enqueued asynchronously on `stream` (a hipStream_t; NULL is
+ *     the null stream).  Nothing synchronises the host.
+ *   - Arguments are checked before anything is enqueued.  On an error the
+ *     call returns a nonzero dptq_status and enqueues nothing.  A failed
+ *     kernel launch returns DPTQ_ERR_HIP.
+ *   - Device pointers must be 16-byte aligned.  Matrices are row-major and
+ *     dense (row stride = row length).
+ *   - Rotation B_h = I_{K/h} (x) H_h is unnormalised (+-1 entries).  H_h is
+ *     Sylvester's natural-order matrix for h = 2^j and H_28 (x) H_{2^j}
+ *     (Paley construction II, q = 13, on the slow index) for h = 28 * 2^j.
+ *     The 1/h that makes (xB)(WB)^T = h X W^T is folded into the weight
+ *     scales by dptq_prepare_weights.
+ *   - Inputs must be finite; codes for rows holding Inf or NaN are
+ *     unspecified.
+ */
+#ifndef DPTQ_H
+#define DPTQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DPTQ_OK = 0,
+  DPTQ_ERR_INVALID_ARG = 1, /* null pointer, negative size, bad bits, ... */
+  DPTQ_ERR_UNSUPPORTED = 2, /* well-formed but outside what the kernels cover */
+  DPTQ_ERR_HIP = 3          /* the HIP runtime reported an error */
+} dptq_status;
+
+/* Largest supported reduction length K (bounds the int32 accumulator). */
+#define DPTQ_MAX_K 65536
+
+/* Static description of a status code (never NULL). */
+const char* dptq_status_string(int status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int dptq_version(void);
+
+/*
+ * dptq_rotate_quant - online rotation + per-token symmetric quantization.
+ * Section 2 Eq. 4 (quantize X R), Eq. 1-2 in symmetric form (Section 4.2).
+ *
+ * For each token row m of x:
+ *   y      = x_m . B_h                  in fp32, pinned order: radix-2
+ *            butterflies over index bit 0, 1, 2, ... of the 2^j factor, then
+ *            (for 28 * 2^j) a sequential sum over the 28-point index a = 0..27
+ *   s_m    = fl32(max_k |y_k| / qmax),  qmax = 7 (bits 4) or 127 (bits 8)
+ *   code_k = clamp(rne(fl32(y_k / s_m)), -2^(bits-1), 2^(bits-1) - 1)
+ *   (s_m = 0 and all codes 0 when the row is all zero)
+ *
+ *   x        device, fp16 [M, K]
+ *   M        tokens, >= 0 (M = 0 enqueues nothing and returns DPTQ_OK)
+ *   K        features, 1 <= K <= DPTQ_MAX_K, multiple of 8 and of had_size;
+ *            K <= 36864 (the row is staged in on-chip memory)
+ *   had_size h in {2^j : 1 <= 2^j <= 32768} or {28 * 2^j : 28*2^j <= 32768}
+ *   bits     4 or 8
+ *   codes    device: bits 4 -> uint8 [M, K/2], byte j = code[2j] (low nibble)
+ *            | code[2j+1] << 4 (4-bit two's complement);
+ *            bits 8 -> int8 [M, K]
+ *   a_scales device, float [M] (s_m)
+ */
+int dptq_rotate_quant(const void* x, int64_t M, int64_t K, int32_t had_size,
+                      int32_t bits, void* codes, float* a_scales, void* stream);
+
+/*
+ * dptq_qlinear - quantized linear: exact integer GEMM + dequant epilogue.
+ * Section 2 (Y = X W^T with W [out, in]), Eq. 5 (pre-rotated weights),
+ * Section 4.2 (per-token activation and per-channel weight scales).
+ *
+ *   acc[m,n] = sum_k a_code[m,k] * w_code[n,k]          (exact, int32)
+ *   y[m,n]   = fl16(fl32(fl32(fl32(acc) * a_scales[m]) * w_scales[n]))
+ *
+ *   codes    device, activation codes in the dptq_rotate_quant layout
+ *   a_scales device, float [M]
+ *   M        tokens >= 0; M <= 16 runs the weight-streaming decode kernel,
+ *            larger M the MFMA tile kernel (same results bit for bit)
+ *   K        multiple of 128, 128 <= K <= DPTQ_MAX_K
+ *   bits     activation bits, 4 or 8
+ *   w_packed device, uint8 [N, K/2]: 4-bit weight codes, same nibble layout as
+ *            4-bit activation codes (as written by dptq_prepare_weights)
+ *   w_scales device, float [N]
+ *   N        output features, multiple of 16, >= 16
+ *   y        device, fp16 [M, N]
+ */
+int dptq_qlinear(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                 int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                 int64_t N, void* y, void* stream);
+
+/*
+ * dptq_qlinear_acc - the same GEMM as dptq_qlinear, writing the raw int32
+ * accumulators acc[m,n] (device, int32 [M, N]) instead of y.  Exposes the
+ * exact integer result for verification; same argument rules.
+ */
+int dptq_qlinear_acc(const void* codes, int64_t M, int64_t K, int32_t bits,
+                     const uint8_t* w_packed, int64_t N, int32_t* acc,
+                     void* stream);
+
+/*
+ * dptq_layer_policy - phase-aware activation precision (host only).
+ * Algorithm 1 step 2 with the sensitive set of Eq. 21.
+ *
+ *   bits_out[l] = 8 if layer l is sensitive else 4, for l = 0 .. num_layers-1.
+ *   mask == NULL: the paper's default S = {1, 2, 3, L} (1-indexed), i.e.
+ *                 {0, 1, 2, L-1} 0-indexed.
+ *   mask != NULL: host uint8 [num_layers]; mask[l] != 0 marks layer l.
+ *   num_layers >= 1; bits_out host int32 [num_layers].
+ */
+int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out);
+
+/*
+ * dptq_prepare_weights - offline weight preparation (Eq. 5 absorption,
+ * per-output-channel symmetric round-to-nearest at 4 bits, Section 4.2).
+ *
+ * For each output row n of w: z = w_n . B_h (same rotation and order as
+ * dptq_rotate_quant, on fp32 input), s = fl32(max|z| / 7), codes as in
+ * dptq_rotate_quant at 4 bits, and w_scales[n] = fl32(s / h).
+ *
+ *   w        device, float [N, K]
+ *   N        >= 0; K, had_size as for dptq_rotate_quant
+ *   w_packed device, uint8 [N, K/2]
+ *   w_scales device, float [N]
+ */
+int dptq_prepare_weights(const float* w, int64_t N, int64_t K, int32_t had_size,
+                         uint8_t* w_packed, float* w_scales, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPTQ_H */

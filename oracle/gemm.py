@@ -7,8 +7,10 @@ channel weight scales (Section 4.2).
 
 Readings:
 * The accumulator is the exact integer sum acc[m, n] = sum_k a[m, k] * w[n, k]
-  (taken here in int64; |acc| <= K * 128 * 8 stays far below 2^31 for every
-  supported K, so a 32-bit accumulator is exact as well).
+  (|acc| <= K * 128 * 8 stays far below 2^31 for every supported K, so a
+  32-bit accumulator is exact as well).  It is formed with a float64 library
+  matmul on the integer codes: every product and partial sum is an integer
+  below 2^53, so the result is exact in any summation order.
 * Epilogue order: y = fl16(fl32(fl32(fl32(acc) * a_s[m]) * w_s[n])), every
   conversion and product rounded to nearest-even.
 """
@@ -34,7 +36,10 @@ def qlinear_acc_ref(a_codes, bits, w_packed):
     w = unpack_int4(w_packed).astype(np.int64)
     if a.shape[1] != w.shape[1]:
         raise ValueError("K mismatch between activation codes and weights")
-    return a @ w.T
+    K = a.shape[1]
+    if K * 128 * 8 >= 2 ** 53:
+        raise ValueError("K too large for an exact float64 accumulation")
+    return (a.astype(np.float64) @ w.astype(np.float64).T).astype(np.int64)
 
 
 def qlinear_acc_entries(a_codes, bits, w_packed, rows, cols):

@@ -30,7 +30,8 @@ import functools
 
 import numpy as np
 
-__all__ = ["sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows"]
+__all__ = ["sylvester", "sylvester_columns", "paley28", "hadamard", "split_had_size",
+           "rotate_rows"]
 
 
 def sylvester(n):
@@ -55,11 +56,14 @@ def _sylvester_i8(n):
     return H
 
 
-@functools.lru_cache(maxsize=8)
-def _sylvester_f32(n):
-    H = _sylvester_i8(n).astype(np.float32)
-    H.setflags(write=False)
-    return H
+def sylvester_columns(n, d0, d1):
+    """Columns d0..d1-1 of the natural-order Sylvester matrix of order n, fp32,
+    from the closed form H[c, d] = (-1)^popcount(c AND d) (equal to the
+    recursive construction; used so large orders never materialise n x n)."""
+    c = np.arange(n, dtype=np.uint32)[:, None]
+    d = np.arange(d0, d1, dtype=np.uint32)[None, :]
+    parity = np.bitwise_count(c & d) & 1
+    return (1 - 2 * parity.astype(np.int8)).astype(np.float32)
 
 
 def _quadratic_character(a, q):
@@ -115,14 +119,29 @@ def _tree_sum_axis0(P):
     return P[0]
 
 
-def _rotate_block_fast_index(xa, Hp, chunk_elems=1 << 22):
-    """z[d] = sum_c xa[c] * Hp[c, d], pairwise tree over c (fp32)."""
-    p = xa.shape[0]
-    z = np.empty(p, dtype=np.float32)
+@functools.lru_cache(maxsize=4)
+def _column_chunks(p, chunk_elems=1 << 22):
     cols = max(1, chunk_elems // p)
+    out = []
     for d0 in range(0, p, cols):
         d1 = min(p, d0 + cols)
-        P = xa[:, None] * Hp[:, d0:d1]          # exact: Hp entries are +-1
+        H = sylvester_columns(p, d0, d1)
+        H.setflags(write=False)
+        out.append((d0, d1, H))
+    return tuple(out) if p * p <= (1 << 26) else None
+
+
+def _rotate_block_fast_index(xa, p, chunk_elems=1 << 22):
+    """z[d] = sum_c xa[c] * H_p[c, d], pairwise tree over c (fp32)."""
+    z = np.empty(p, dtype=np.float32)
+    chunks = _column_chunks(p)
+    if chunks is None:   # large orders: regenerate columns instead of caching them
+        cols = max(1, chunk_elems // p)
+        chunks = ((d0, min(p, d0 + cols), None) for d0 in range(0, p, cols))
+    for d0, d1, H in chunks:
+        if H is None:
+            H = sylvester_columns(p, d0, d1)
+        P = xa[:, None] * H                     # exact: entries are +-1
         z[d0:d1] = _tree_sum_axis0(P)
     return z
 
@@ -140,13 +159,12 @@ def rotate_rows(x, h):
     if K % h != 0:
         raise ValueError(f"K={K} is not a multiple of the Hadamard size {h}")
     x32 = x.astype(np.float32)                   # fp16 -> fp32 is exact
-    Hp = _sylvester_f32(p)
     H28 = paley28().astype(np.float32) if f == 28 else None
     y = np.empty((M, K), dtype=np.float32)
     for m in range(M):
         for blk in range(K // h):
             xb = x32[m, blk * h:(blk + 1) * h].reshape(f, p)   # i = a*p + c
-            z = np.stack([_rotate_block_fast_index(xb[a], Hp) for a in range(f)])
+            z = np.stack([_rotate_block_fast_index(xb[a], p) for a in range(f)])
             if f == 1:
                 out = z[0]
             else:

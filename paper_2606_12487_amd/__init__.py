@@ -1,0 +1,211 @@
+"""Python binding of libdptq, the MI355X quantized linear layer of DynamicPTQ.
+
+Thin ctypes marshalling over the C ABI declared in ``include/dptq.h``: the
+functions below check tensor dtypes and shapes, allocate outputs with torch
+(device memory and streams only) and call the library on the current HIP
+stream.  Every arithmetic step runs in the library's kernels; there is no
+fallback path, and importing a function whose library is missing raises.
+
+    codes, scales = rotate_quant(x_fp16, had_size=4096, bits=4)
+    w_packed, w_scales = prepare_weights(w_fp32, had_size=4096)
+    y = qlinear(codes, scales, 4, w_packed, w_scales)
+"""
+
+import ctypes
+import os
+
+__all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
+           "layer_policy", "prepare_weights", "version", "EXPORTED_FUNCTIONS"]
+
+_PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+_LIB_NAME = "libdptq.so"
+_lib = None
+
+# Every function the C ABI exports (include/dptq.h).
+EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
+                      "dptq_qlinear", "dptq_qlinear_acc", "dptq_layer_policy",
+                      "dptq_prepare_weights")
+
+
+class DptqError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {_status_string(status)} (status {status})")
+
+
+def library_path():
+    return os.path.join(_PKG_DIR, _LIB_NAME)
+
+
+def lib():
+    """The loaded libdptq (ctypes.CDLL).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(
+                f"{path} is missing: build it with `python -m paper_2606_12487_amd.build` "
+                "(the HIP library is required; there is no fallback)")
+        L = ctypes.CDLL(path)
+        i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+        L.dptq_status_string.argtypes = [ctypes.c_int]
+        L.dptq_status_string.restype = ctypes.c_char_p
+        L.dptq_version.argtypes = []
+        L.dptq_version.restype = ctypes.c_int
+        L.dptq_rotate_quant.argtypes = [vp, i64, i64, i32, i32, vp, vp, vp]
+        L.dptq_rotate_quant.restype = ctypes.c_int
+        L.dptq_qlinear.argtypes = [vp, vp, i64, i64, i32, vp, vp, i64, vp, vp]
+        L.dptq_qlinear.restype = ctypes.c_int
+        L.dptq_qlinear_acc.argtypes = [vp, i64, i64, i32, vp, i64, vp, vp]
+        L.dptq_qlinear_acc.restype = ctypes.c_int
+        L.dptq_layer_policy.argtypes = [i32, vp, vp]
+        L.dptq_layer_policy.restype = ctypes.c_int
+        L.dptq_prepare_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp]
+        L.dptq_prepare_weights.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _status_string(status):
+    try:
+        return lib().dptq_status_string(int(status)).decode()
+    except Exception:  # pragma: no cover - library unavailable
+        return "unknown"
+
+
+def version():
+    return lib().dptq_version()
+
+
+def _check(status, what):
+    if status != 0:
+        raise DptqError(status, what)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(t):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _require(t, name, dtype, shape=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def code_shape(M, K, bits):
+    return (M, K // 2) if bits == 4 else (M, K)
+
+
+def rotate_quant(x, had_size, bits, codes=None, scales=None):
+    """Rotate (I (x) H_h) and quantize fp16 rows x [M, K] -> (codes, fp32 scales [M])."""
+    torch = _torch()
+    _require(x, "x", torch.float16)
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [M, K]")
+    M, K = x.shape
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    cdt = torch.uint8 if bits == 4 else torch.int8
+    if codes is None:
+        codes = torch.empty(code_shape(M, K, bits), dtype=cdt, device=x.device)
+    _require(codes, "codes", cdt, code_shape(M, K, bits))
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=x.device)
+    _require(scales, "scales", torch.float32, (M,))
+    _check(lib().dptq_rotate_quant(_ptr(x), M, K, int(had_size), int(bits), _ptr(codes),
+                                   _ptr(scales), _stream(x)), "dptq_rotate_quant")
+    return codes, scales
+
+
+def _gemm_args(codes, bits, w_packed):
+    torch = _torch()
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    cdt = torch.uint8 if bits == 4 else torch.int8
+    _require(codes, "codes", cdt)
+    _require(w_packed, "w_packed", torch.uint8)
+    M = codes.shape[0]
+    K = codes.shape[1] * (2 if bits == 4 else 1)
+    N = w_packed.shape[0]
+    if w_packed.shape[1] * 2 != K:
+        raise ValueError(f"w_packed must be [N, K/2] with K = {K}")
+    return M, K, N
+
+
+def qlinear(codes, a_scales, bits, w_packed, w_scales, y=None):
+    """y [M, N] fp16 = dequant(codes . w^T) with per-token x per-channel scales."""
+    torch = _torch()
+    M, K, N = _gemm_args(codes, bits, w_packed)
+    _require(a_scales, "a_scales", torch.float32, (M,))
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
+    _require(y, "y", torch.float16, (M, N))
+    _check(lib().dptq_qlinear(_ptr(codes), _ptr(a_scales), M, K, int(bits), _ptr(w_packed),
+                              _ptr(w_scales), N, _ptr(y), _stream(codes)), "dptq_qlinear")
+    return y
+
+
+def qlinear_acc(codes, bits, w_packed, acc=None):
+    """Raw int32 accumulators acc [M, N] = codes . w^T (exact)."""
+    torch = _torch()
+    M, K, N = _gemm_args(codes, bits, w_packed)
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=codes.device)
+    _require(acc, "acc", torch.int32, (M, N))
+    _check(lib().dptq_qlinear_acc(_ptr(codes), M, K, int(bits), _ptr(w_packed), N, _ptr(acc),
+                                  _stream(codes)), "dptq_qlinear_acc")
+    return acc
+
+
+def layer_policy(num_layers, mask=None):
+    """Activation bits per layer (Eq. 21 default set, or the layers a mask marks)."""
+    L = int(num_layers)
+    out = (ctypes.c_int32 * max(L, 1))()
+    if mask is None:
+        mptr = ctypes.c_void_p(0)
+    else:
+        m = [1 if v else 0 for v in mask]
+        if len(m) != L:
+            raise ValueError("mask length must equal num_layers")
+        buf = (ctypes.c_uint8 * max(L, 1))(*m)
+        mptr = ctypes.cast(buf, ctypes.c_void_p)
+    _check(lib().dptq_layer_policy(L, mptr, ctypes.cast(out, ctypes.c_void_p)),
+           "dptq_layer_policy")
+    return [int(v) for v in out[:L]]
+
+
+def prepare_weights(w, had_size, w_packed=None, w_scales=None):
+    """Offline: rotate, quantize to 4 bits per output channel and pack fp32 w [N, K]."""
+    torch = _torch()
+    _require(w, "w", torch.float32)
+    if w.dim() != 2:
+        raise ValueError("w must be 2-D [N, K]")
+    N, K = w.shape
+    if w_packed is None:
+        w_packed = torch.empty((N, K // 2), dtype=torch.uint8, device=w.device)
+    _require(w_packed, "w_packed", torch.uint8, (N, K // 2))
+    if w_scales is None:
+        w_scales = torch.empty((N,), dtype=torch.float32, device=w.device)
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    _check(lib().dptq_prepare_weights(_ptr(w), N, K, int(had_size), _ptr(w_packed),
+                                      _ptr(w_scales), _stream(w)), "dptq_prepare_weights")
+    return w_packed, w_scales

@@ -1,0 +1,136 @@
+// C ABI: argument checks, then dispatch to the gfx950 kernels.
+#include "dptq.h"
+#include "internal.h"
+
+namespace {
+
+using dptq::HadSplit;
+
+constexpr int kVersion = 100;  // 0.1.0
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// h = 2^j or 28 * 2^j with h <= 32768.
+bool split_had(int64_t h, HadSplit* out) {
+  if (h < 1 || h > 32768) return false;
+  if ((h & (h - 1)) == 0) {
+    int j = 0;
+    while ((int64_t{1} << j) < h) ++j;
+    *out = HadSplit{1, j};
+    return true;
+  }
+  if (h % 28 == 0) {
+    const int64_t p = h / 28;
+    if ((p & (p - 1)) == 0) {
+      int j = 0;
+      while ((int64_t{1} << j) < p) ++j;
+      *out = HadSplit{28, j};
+      return true;
+    }
+  }
+  return false;
+}
+
+int check_rotation_shape(int64_t M, int64_t K, int32_t had_size, HadSplit* hs) {
+  if (M < 0 || K < 1) return DPTQ_ERR_INVALID_ARG;
+  if (!split_had(had_size, hs)) return DPTQ_ERR_INVALID_ARG;
+  if (K % had_size != 0 || K % 8 != 0) return DPTQ_ERR_INVALID_ARG;
+  if (K > dptq::kMaxRotateK) return DPTQ_ERR_UNSUPPORTED;
+  if (M > 0x7FFFFFFF) return DPTQ_ERR_UNSUPPORTED;
+  return DPTQ_OK;
+}
+
+int check_gemm_shape(int64_t M, int64_t K, int32_t bits, int64_t N) {
+  if (M < 0 || K < 1 || N < 1) return DPTQ_ERR_INVALID_ARG;
+  if (bits != 4 && bits != 8) return DPTQ_ERR_INVALID_ARG;
+  if (K % 128 != 0 || K > DPTQ_MAX_K) return DPTQ_ERR_UNSUPPORTED;
+  if (N % 16 != 0 || N > 0x7FFFFFF0) return DPTQ_ERR_UNSUPPORTED;
+  if (M > 0x7FFFFFFF) return DPTQ_ERR_UNSUPPORTED;
+  if ((M > 16) && ((M + 127) / 128) * ((N + 255) / 256) > 0x7FFFFFFF) return DPTQ_ERR_UNSUPPORTED;
+  return DPTQ_OK;
+}
+
+int from_hip(hipError_t e) { return e == hipSuccess ? DPTQ_OK : DPTQ_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* dptq_status_string(int status) {
+  switch (status) {
+    case DPTQ_OK: return "ok";
+    case DPTQ_ERR_INVALID_ARG: return "invalid argument";
+    case DPTQ_ERR_UNSUPPORTED: return "unsupported shape or size";
+    case DPTQ_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int dptq_version(void) { return kVersion; }
+
+int dptq_rotate_quant(const void* x, int64_t M, int64_t K, int32_t had_size, int32_t bits,
+                      void* codes, float* a_scales, void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(M, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (bits != 4 && bits != 8) return DPTQ_ERR_INVALID_ARG;
+  if (M == 0) return DPTQ_OK;
+  if (!x || !codes || !a_scales) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(codes) || !aligned16(a_scales)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_rotate_quant_f16(x, M, (int)K, hs, bits, codes, a_scales,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+int dptq_qlinear(const void* codes, const float* a_scales, int64_t M, int64_t K, int32_t bits,
+                 const uint8_t* w_packed, const float* w_scales, int64_t N, void* y,
+                 void* stream) {
+  int st = check_gemm_shape(M, K, bits, N);
+  if (st != DPTQ_OK) return st;
+  if (M == 0) return DPTQ_OK;
+  if (!codes || !a_scales || !w_packed || !w_scales || !y) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(a_scales) || !aligned16(w_packed) ||
+      !aligned16(w_scales) || !aligned16(y))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_qlinear(codes, a_scales, M, (int)K, bits, w_packed, w_scales, N,
+                                       y, nullptr, static_cast<hipStream_t>(stream)));
+}
+
+int dptq_qlinear_acc(const void* codes, int64_t M, int64_t K, int32_t bits,
+                     const uint8_t* w_packed, int64_t N, int32_t* acc, void* stream) {
+  int st = check_gemm_shape(M, K, bits, N);
+  if (st != DPTQ_OK) return st;
+  if (M == 0) return DPTQ_OK;
+  if (!codes || !w_packed || !acc) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(w_packed) || !aligned16(acc)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_qlinear(codes, nullptr, M, (int)K, bits, w_packed, nullptr, N,
+                                       nullptr, acc, static_cast<hipStream_t>(stream)));
+}
+
+int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {
+  if (num_layers < 1 || !bits_out) return DPTQ_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < num_layers; ++l) {
+    bool sensitive;
+    if (mask) {
+      sensitive = mask[l] != 0;
+    } else {
+      // Eq. 21: S = {1, 2, 3, L} counted from 1, i.e. {0, 1, 2, L-1}.
+      sensitive = l <= 2 || l == num_layers - 1;
+    }
+    bits_out[l] = sensitive ? 8 : 4;
+  }
+  return DPTQ_OK;
+}
+
+int dptq_prepare_weights(const float* w, int64_t N, int64_t K, int32_t had_size,
+                         uint8_t* w_packed, float* w_scales, void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(N, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (N == 0) return DPTQ_OK;
+  if (!w || !w_packed || !w_scales) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(w) || !aligned16(w_packed) || !aligned16(w_scales)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_prepare_weights(w, N, (int)K, hs, w_packed, w_scales,
+                                               static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,32 @@
+// Internal declarations shared by the C-ABI layer and the kernel sources.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+namespace dptq {
+
+// Hadamard size h = f * 2^j with f in {1, 28}.
+struct HadSplit {
+  int f;      // 1 or 28
+  int j;      // log2 of the power-of-two factor
+};
+
+// Largest row the rotate-quant kernel stages on chip (fp32 + padding < 160 KiB).
+constexpr int kMaxRotateK = 36864;
+
+// Launchers return hipSuccess or the launch error; arguments are already valid.
+hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
+                                   int bits, void* codes, float* scales,
+                                   hipStream_t stream);
+hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
+                                  uint8_t* w_packed, float* w_scales,
+                                  hipStream_t stream);
+// out_acc != nullptr selects the raw int32 accumulator output.
+hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
+                          int K, int bits, const uint8_t* w_packed,
+                          const float* w_scales, int64_t N, void* y,
+                          int32_t* out_acc, hipStream_t stream);
+
+}  // namespace dptq

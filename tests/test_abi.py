@@ -1,0 +1,143 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+The library must load, export every function include/dptq.h declares, run the
+host-only policy exactly as the oracle does, and reject every invalid argument
+before anything is enqueued (so these calls never touch a GPU).
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_12487_amd as dptq
+from oracle.policy import layer_policy_ref
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dptq.h")
+
+OK, INVALID, UNSUPPORTED, HIPERR = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(0x10000)           # aligned, never dereferenced
+MISALIGNED = ctypes.c_void_p(0x10004)
+NULL = ctypes.c_void_p(0)
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dptq_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(dptq.library_path()):
+        import __graft_entry__
+        __graft_entry__.build()
+    return dptq.lib()
+
+
+def test_header_and_binding_agree():
+    assert _declared_functions() == sorted(dptq.EXPORTED_FUNCTIONS)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in _declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_status_strings_and_version(L):
+    for st in (OK, INVALID, UNSUPPORTED, HIPERR):
+        assert L.dptq_status_string(st)
+    assert L.dptq_status_string(99) == b"unknown status"
+    assert dptq.version() >= 100
+
+
+@pytest.mark.parametrize("L_layers", [1, 2, 3, 4, 5, 28, 32, 40, 80])
+def test_policy_default_matches_oracle(L, L_layers):
+    assert dptq.layer_policy(L_layers) == layer_policy_ref(L_layers)
+
+
+def test_policy_mask_matches_oracle(L):
+    import workloads
+    for Ls, seed in ((32, 3), (80, 5)):
+        mask = workloads.layer_mask(Ls, 4, seed)
+        assert dptq.layer_policy(Ls, mask) == layer_policy_ref(Ls, list(mask))
+        assert sum(b == 8 for b in dptq.layer_policy(Ls, mask)) == 4
+
+
+def test_policy_rejects_bad_args(L):
+    out = (ctypes.c_int32 * 4)()
+    assert L.dptq_layer_policy(0, NULL, ctypes.cast(out, ctypes.c_void_p)) == INVALID
+    assert L.dptq_layer_policy(4, NULL, NULL) == INVALID
+
+
+def rq(L, x=FAKE, M=4, K=256, h=256, bits=4, codes=FAKE, scales=FAKE):
+    return L.dptq_rotate_quant(x, M, K, h, bits, codes, scales, NULL)
+
+
+def test_rotate_quant_validation(L):
+    assert rq(L, bits=5) == INVALID
+    assert rq(L, bits=0) == INVALID
+    assert rq(L, M=-1) == INVALID
+    assert rq(L, K=0) == INVALID
+    assert rq(L, h=12) == INVALID            # not 2^j or 28 * 2^j
+    assert rq(L, h=0) == INVALID
+    assert rq(L, h=65536, K=65536) == INVALID
+    assert rq(L, K=384, h=256) == INVALID   # h does not divide K
+    assert rq(L, K=28 * 9, h=28) == INVALID  # K not a multiple of 8
+    assert rq(L, K=36864 + 256, h=256) == UNSUPPORTED
+    assert rq(L, x=NULL) == INVALID
+    assert rq(L, codes=NULL) == INVALID
+    assert rq(L, scales=NULL) == INVALID
+    assert rq(L, x=MISALIGNED) == INVALID
+    assert rq(L, codes=MISALIGNED) == INVALID
+    # M = 0 is a valid empty call: nothing is enqueued, pointers may be null
+    assert rq(L, M=0, x=NULL, codes=NULL, scales=NULL) == OK
+
+
+def ql(L, codes=FAKE, a_s=FAKE, M=32, K=256, bits=4, w=FAKE, w_s=FAKE, N=64, y=FAKE):
+    return L.dptq_qlinear(codes, a_s, M, K, bits, w, w_s, N, y, NULL)
+
+
+def test_qlinear_validation(L):
+    assert ql(L, bits=2) == INVALID
+    assert ql(L, M=-3) == INVALID
+    assert ql(L, N=0) == INVALID
+    assert ql(L, K=0) == INVALID
+    assert ql(L, K=192) == UNSUPPORTED       # K % 128
+    assert ql(L, K=65536 + 128) == UNSUPPORTED
+    assert ql(L, N=72) == UNSUPPORTED        # N % 16
+    for name in ("codes", "a_s", "w", "w_s", "y"):
+        assert ql(L, **{name: NULL}) == INVALID, name
+        assert ql(L, **{name: MISALIGNED}) == INVALID, name
+    assert ql(L, M=0, codes=NULL, a_s=NULL, w=NULL, w_s=NULL, y=NULL) == OK
+
+
+def test_qlinear_acc_validation(L):
+    f = L.dptq_qlinear_acc
+    assert f(FAKE, 8, 256, 3, FAKE, 64, FAKE, NULL) == INVALID
+    assert f(NULL, 8, 256, 4, FAKE, 64, FAKE, NULL) == INVALID
+    assert f(FAKE, 8, 256, 4, NULL, 64, FAKE, NULL) == INVALID
+    assert f(FAKE, 8, 256, 4, FAKE, 64, NULL, NULL) == INVALID
+    assert f(FAKE, 8, 200, 4, FAKE, 64, FAKE, NULL) == UNSUPPORTED
+    assert f(FAKE, 0, 256, 8, NULL, 64, NULL, NULL) == OK
+
+
+def test_prepare_weights_validation(L):
+    f = L.dptq_prepare_weights
+    assert f(FAKE, 16, 256, 100, FAKE, FAKE, NULL) == INVALID
+    assert f(NULL, 16, 256, 256, FAKE, FAKE, NULL) == INVALID
+    assert f(FAKE, 16, 256, 256, MISALIGNED, FAKE, NULL) == INVALID
+    assert f(FAKE, -1, 256, 256, FAKE, FAKE, NULL) == INVALID
+    assert f(NULL, 0, 256, 256, NULL, NULL, NULL) == OK
+
+
+def test_python_wrappers_check_tensors():
+    torch = pytest.importorskip("torch")
+    with pytest.raises(TypeError):
+        dptq.rotate_quant(torch.zeros(4, 256, dtype=torch.float32), 256, 4)
+    with pytest.raises(ValueError):
+        dptq.rotate_quant(torch.zeros(4, 256, dtype=torch.float16), 256, 4)  # not on GPU
+    with pytest.raises(ValueError):
+        dptq.layer_policy(3, [1, 0])

@@ -11,7 +11,8 @@ import pytest
 import scipy.linalg
 
 import oracle
-from oracle.hadamard import paley28, sylvester, hadamard, rotate_rows, split_had_size
+from oracle.hadamard import (paley28, sylvester, sylvester_columns, hadamard,
+                             rotate_rows, split_had_size)
 
 POW2 = [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096]
 
@@ -20,6 +21,17 @@ POW2 = [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096]
 def test_sylvester_matches_scipy(n):
     # scipy.linalg.hadamard builds the same natural-order Sylvester matrix.
     assert np.array_equal(sylvester(n), scipy.linalg.hadamard(n).astype(np.int64))
+
+
+@pytest.mark.parametrize("n", POW2)
+def test_closed_form_columns_match_recursion(n):
+    # The rotation draws column chunks from (-1)^popcount(c & d); it must be
+    # the recursive Sylvester matrix.
+    H = sylvester(n)
+    assert np.array_equal(sylvester_columns(n, 0, n).astype(np.int64), H)
+    if n >= 4:
+        assert np.array_equal(sylvester_columns(n, n // 4, n // 2).astype(np.int64),
+                              H[:, n // 4:n // 2])
 
 
 def test_paley28_is_hadamard():

@@ -124,3 +124,21 @@ def activations_for(name, M=None, seed=None):
     if kind == "student_t":
         return student_t(rng, M, K)
     raise ValueError(kind)
+
+
+def random_code_bytes(rng, M, K, bits):
+    """Seeded activation code buffers for GEMM tests: 4-bit -> uint8 [M, K/2]
+    (every byte is a valid pair of nibbles), 8-bit -> int8 [M, K] in [-127, 127]."""
+    if bits == 4:
+        return rng.integers(0, 256, size=(M, K // 2), dtype=np.uint8)
+    return rng.integers(-127, 128, size=(M, K), dtype=np.int8)
+
+
+def random_weight_bytes(rng, N, K):
+    """Seeded packed 4-bit weight buffer uint8 [N, K/2]."""
+    return rng.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+
+
+def random_scales(rng, n, lo=1e-4, hi=1e-1):
+    """Seeded positive fp32 scales."""
+    return rng.uniform(lo, hi, n).astype(np.float32)
