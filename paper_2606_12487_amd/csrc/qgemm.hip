@@ -77,17 +77,58 @@ __device__ __forceinline__ __half dequant(int acc, float as, float ws) {
 }
 
 // ---------------------------------------------------------------------------
-// Prefill: 256 (n) x 128 (m) tiles, 4 wavefronts of 128 (n) x 64 (m), K steps
-// of 128 staged in double-buffered LDS.
+// Prefill: 256 (n) x 128 (m) output tiles on 8 wavefronts (two per SIMD) of
+// 64 (n) x 64 (m), each a 2 x 2 grid of 32 x 32 x 32 int8 MFMAs.  K is consumed in stages of
+// 256 (128-byte row slices for 4-bit operands, so every global request is a
+// full cache line) through two LDS buffers filled by direct global->LDS
+// 16-byte loads; the next stage streams in while the current one is
+// computed.  The fp16 tile is staged through LDS so that the output rows are
+// written with coalesced 16-byte stores.
 // ---------------------------------------------------------------------------
-constexpr int kBN = 256, kBM = 128, kBK = 128, kThreads = 256;
+constexpr int kBN = 256, kBM = 128, kBK = 256;
+// Wavefront grid and per-wavefront MFMA tiles (32 x 32 each).
+constexpr int kWN = 4, kWM = 2;              // wavefronts along n and m
+constexpr int kTI = kBN / kWN / 32;          // 32-row n tiles per wavefront (2)
+constexpr int kTJ = kBM / kWM / 32;          // 32-row m tiles per wavefront (2)
+constexpr int kWaves = kWN * kWM, kThreads = kWaves * 64;
 
-template <int BITS>
-struct TileLds {
-  static constexpr int kW = kBN * (kBK / 2);                     // bytes per W stage
-  static constexpr int kA = kBM * (BITS == 4 ? kBK / 2 : kBK);   // bytes per A stage
-  static constexpr int kStage = kW + kA;
-};
+typedef __attribute__((address_space(3))) uint8_t* lds_ptr;
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+// One wavefront-wide 16-byte-per-lane direct load from global memory into LDS
+// at byte offset lds_off (+ 16 * lane).  Issued as asm so that the compiler's
+// conservative wait (it cannot tell the two buffers apart) does not drain
+// the loads before every LDS read; completion is tracked with wait_vmcnt.
+// Address = wavefront-uniform base + 32-bit per-lane offset.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_off)
+               : "memory", "m0");
+}
+
+// Workgroup barrier without the release/acquire fences of __syncthreads(): the
+// fences would drain every outstanding direct-to-LDS load.  Callers wait for
+// exactly the loads they need with wait_vmcnt first; the asm clobber keeps LDS
+// accesses on their side.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// s_waitcnt vmcnt(N) (gfx9 encoding), leaving the other counters untouched.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ v16i mfma32(v4i a, v4i b, v16i c) {
+  return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// XOR swizzle of the 16-byte chunks of an LDS tile row so that the fragment
+// reads (consecutive rows, one logical chunk per 8- or 16-lane group) hit
+// distinct banks: rows of 8 chunks (128 B) and of 16 chunks (256 B).
+__device__ __forceinline__ int swz8(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int swz16(int r) { return r & 15; }
 
 __device__ __forceinline__ int xcd_remap(int bid, int total) {
   const int per = total >> 3, rem = total & 7;
@@ -95,13 +136,26 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
   return x * per + (x < rem ? x : rem) + idx;
 }
 
+template <int BITS>
+struct Tile {
+  static constexpr int kWRow = kBK / 2;                        // 128 B
+  static constexpr int kARow = BITS == 4 ? kBK / 2 : kBK;      // 128 or 256 B
+  static constexpr int kW = kBN * kWRow;                       // 32 KiB
+  static constexpr int kA = kBM * kARow;                       // 16 or 32 KiB
+  static constexpr int kStage = kW + kA;
+  static constexpr int kWLoads = kW / 1024 / kWaves;           // per wavefront
+  static constexpr int kALoads = kA / 1024 / kWaves;
+  static constexpr int kOutStride = kBN * 2 + 16;              // fp16 output row in LDS
+  static_assert(kBM * kOutStride <= 2 * kStage, "output staging must fit the ring");
+};
+
 template <int BITS, bool ACC_OUT>
 __global__ void __launch_bounds__(kThreads)
 qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
               const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
               int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
-  using L = TileLds<BITS>;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * L::kStage];
+  using T = Tile<BITS>;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * T::kStage];
 
   const int tiles_m = (M + kBM - 1) / kBM;
   const int tiles_n = N / kBN + (N % kBN ? 1 : 0);
@@ -110,137 +164,258 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
   const int m0 = tm * kBM, n0 = tn * kBN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int wn = wave & 1, wm = wave >> 1;
-  const size_t wrow = (size_t)K / 2;
-  const size_t arow = BITS == 4 ? (size_t)K / 2 : (size_t)K;
+  const int wn = wave % kWN, wm = wave / kWN;
+  const int wrow = K / 2;
+  const int arow = BITS == 4 ? K / 2 : K;
+  const int nst = (K + kBK - 1) / kBK;
+  const bool half_tail = (K % kBK) != 0;   // last stage holds only 128 k
 
-  constexpr int kWChunks = L::kW / 16 / kThreads;   // 4
-  constexpr int kAChunks = L::kA / 16 / kThreads;   // 2 (A4) or 4 (A8)
-  uint4 wreg[kWChunks], areg[kAChunks];
-
-  auto gload = [&](int kk) {
-#pragma unroll
-    for (int i = 0; i < kWChunks; ++i) {
-      const int q = t + kThreads * i, r = q >> 2, c = q & 3;
-      const int n = n0 + r;
-      wreg[i] = n < N ? *reinterpret_cast<const uint4*>(w_packed + (size_t)n * wrow + kk / 2 + c * 16)
-                      : make_uint4(0, 0, 0, 0);
+  // Direct loads.  One load instruction fills 1 KiB of LDS: 8 rows of 128 B
+  // (4-bit operands) or 4 rows of 256 B (8-bit activations); lane l writes
+  // physical chunk p of its row, which holds logical chunk p ^ swizzle(row).
+  // Load i of wavefront w fills LDS block i * kWaves + w: rows
+  // (i * kWaves + w) * 8 + (l >> 3) (resp. * 4 + (l >> 4)).  With 8
+  // wavefronts the swizzle of those rows does not depend on i, so the row
+  // part of the address is a wavefront-uniform base and the lane part a single
+  // offset.  Tiles that overhang the matrix clamp rows to the last one, and a
+  // half tail stage (K % 256 == 128) maps chunks past K onto their first-half
+  // twins; both only feed results that are never stored.
+  static_assert(kWaves == 8, "load swizzle assumes 8 wavefronts");
+  constexpr int kARows = BITS == 4 ? 8 : 4;   // rows per A load instruction
+  const bool w_full = n0 + kBN <= N;
+  const bool a_full = m0 + kBM <= M;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);   // known wavefront-uniform
+  uint32_t wlane, alane;
+  {
+    const int rl = lane >> 3;                       // swz8(r) = (rl ^ wave) & 7
+    const int c = ((lane & 7) ^ rl ^ wave) & 7;
+    wlane = (uint32_t)(rl * wrow + c * 16);
+    if (BITS == 4) {
+      alane = (uint32_t)(rl * arow + c * 16);
+    } else {
+      const int r16 = (wave & 3) * 4 + (lane >> 4);   // swz16(r) = r & 15 = r16
+      alane = (uint32_t)((lane >> 4) * arow + ((lane & 15) ^ r16) * 16);
     }
+  }
+  const uint32_t smem_base = (uint32_t)(uintptr_t)(lds_ptr)smem;
+  const uint32_t wave_off = (uint32_t)wave_u * 1024;
+  auto issue = [&](int st, int buf) __attribute__((always_inline)) {
+    const uint32_t base = smem_base + buf * T::kStage + wave_off;
+    const bool tail = half_tail && st == nst - 1;
+    const uint8_t* wt = w_packed + (size_t)n0 * wrow + (size_t)st * T::kWRow;   // uniform
+    const uint8_t* at = a_codes + (size_t)m0 * arow + (size_t)st * T::kARow;    // uniform
+    if (w_full && !tail) {
 #pragma unroll
-    for (int i = 0; i < kAChunks; ++i) {
-      const int q = t + kThreads * i;
-      const int r = BITS == 4 ? (q >> 2) : (q >> 3);
-      const int c = BITS == 4 ? (q & 3) : (q & 7);
-      const int m = m0 + r;
-      const size_t off = BITS == 4 ? (size_t)kk / 2 + c * 16 : (size_t)kk + c * 16;
-      areg[i] = m < M ? *reinterpret_cast<const uint4*>(a_codes + (size_t)m * arow + off)
-                      : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-    uint8_t* ws = smem + buf * L::kStage;
-    uint8_t* as = ws + L::kW;
+      for (int i = 0; i < T::kWLoads; ++i)
+        dma16(wt + (size_t)((i * kWaves + wave_u) * 8) * wrow, wlane, base + i * kWaves * 1024);
+    } else {
 #pragma unroll
-    for (int i = 0; i < kWChunks; ++i)
-      *reinterpret_cast<uint4*>(ws + (t + kThreads * i) * 16) = wreg[i];
-#pragma unroll
-    for (int i = 0; i < kAChunks; ++i) {
-      const int q = t + kThreads * i;
-      int off;
-      if (BITS == 4) {
-        off = q * 16;
-      } else {
-        // [k half][row][16-byte column]: row r, chunk c -> half c & 1
-        const int r = q >> 3, c = q & 7;
-        off = (c & 1) * (kBM * 64) + r * 64 + (c >> 1) * 16;
-      }
-      *reinterpret_cast<uint4*>(as + off) = areg[i];
-    }
-  };
-
-  v4i acc[8][4];
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-
-  const int steps = K / kBK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-
-  const int fr = lane & 15, fg = lane >> 4;
-  for (int s = 0; s < steps; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < steps) gload((s + 1) * kBK);
-    const uint8_t* ws = smem + buf * L::kStage;
-    const uint8_t* as = ws + L::kW;
-
-    uint4 af[4];
-    uint4 af2[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wm * 64 + j * 16 + fr;
-      if (BITS == 4) {
-        af[j] = *reinterpret_cast<const uint4*>(as + r * 64 + fg * 16);
-      } else {
-        af[j] = *reinterpret_cast<const uint4*>(as + r * 64 + fg * 16);
-        af2[j] = *reinterpret_cast<const uint4*>(as + kBM * 64 + r * 64 + fg * 16);
+      for (int i = 0; i < T::kWLoads; ++i) {
+        const int r = (i * kWaves + wave) * 8 + (lane >> 3);
+        int c = (lane & 7) ^ swz8(r);
+        if (tail) c &= 3;
+        const int rc = min(r, N - 1 - n0);
+        dma16(wt, (uint32_t)(rc * wrow + c * 16), base + i * kWaves * 1024);
       }
     }
-    uint4 wf[8];
+    if (a_full && !tail) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = wn * 128 + i * 16 + fr;
-      wf[i] = *reinterpret_cast<const uint4*>(ws + r * 64 + fg * 16);
-    }
+      for (int i = 0; i < T::kALoads; ++i)
+        dma16(at + (size_t)((i * kWaves + wave_u) * kARows) * arow, alane,
+              base + T::kW + i * kWaves * 1024);
+    } else {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      v4i bop[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int i = 0; i < T::kALoads; ++i) {
+        int r, c;
         if (BITS == 4) {
-          bop[j] = ks == 0 ? op_from_nibbles(af[j].x, af[j].y) : op_from_nibbles(af[j].z, af[j].w);
+          r = (i * kWaves + wave) * 8 + (lane >> 3);
+          c = (lane & 7) ^ swz8(r);
+          if (tail) c &= 3;
         } else {
-          bop[j] = ks == 0 ? op_from_bytes(af[j].x, af[j].y, af[j].z, af[j].w)
-                           : op_from_bytes(af2[j].x, af2[j].y, af2[j].z, af2[j].w);
+          r = (i * kWaves + wave) * 4 + (lane >> 4);
+          c = (lane & 15) ^ swz16(r);
+          if (tail) c &= 7;
+        }
+        const int rc = min(r, M - 1 - m0);
+        dma16(at, (uint32_t)(rc * arow + c * 16), base + T::kW + i * kWaves * 1024);
+      }
+    }
+  };
+
+  // Fragment addresses.  In half h (128 k) of a stage, lane l reads row l & 31
+  // of its 32-row tile, k range [128 h + 64 g, +64), g = l >> 5: two 16-byte
+  // chunks of a 4-bit row, four of an 8-bit row.  The tile index enters as an
+  // immediate offset; for 4-bit rows the swizzle of tile i's row differs from
+  // tile 0's by 4 (i & 1), so only [h ^ (i & 1)][e] variants are needed.
+  const int fr = lane & 31, fg = lane >> 5;
+  const int s0 = (fr & 7) ^ (fr >> 3);
+  uint32_t wv[2][2];
+  uint32_t av[2][4];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+      wv[x][e] = (uint32_t)((wn * kTI * 32 + fr) * T::kWRow + (((2 * fg) ^ s0 ^ (4 * x + e)) & 7) * 16);
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (BITS == 4)
+        av[x][e] = e < 2 ? (uint32_t)((wm * kTJ * 32 + fr) * T::kARow + (((2 * fg) ^ s0 ^ (4 * x + e)) & 7) * 16) : 0u;
+      else
+        av[x][e] = (uint32_t)((wm * kTJ * 32 + fr) * T::kARow + (((8 * x + 4 * fg + e) ^ (fr & 15)) & 15) * 16);
+    }
+
+  // A stage is consumed as four chunk pairs p = 2 h + e: the 16-byte chunk e
+  // of half h of every fragment row, i.e. two 32-k MFMA steps.  The packed
+  // fragments of pair p+1 are read from LDS while pair p is unpacked and
+  // multiplied.
+  constexpr int kAD = BITS == 4 ? 4 : 8;
+  struct Frags {
+    uint32_t w[kTI][4];
+    uint32_t a[kTJ][kAD];
+  };
+  auto read_pair = [&](const uint8_t* buf, int h, int e, Frags& f) __attribute__((always_inline)) {
+    const uint8_t* ws = buf;
+    const uint8_t* as = buf + T::kW;
+#pragma unroll
+    for (int i = 0; i < kTI; ++i) {
+      const uint4 v = *reinterpret_cast<const uint4*>(ws + wv[h ^ (i & 1)][e] + i * 32 * T::kWRow);
+      f.w[i][0] = v.x; f.w[i][1] = v.y; f.w[i][2] = v.z; f.w[i][3] = v.w;
+    }
+#pragma unroll
+    for (int j = 0; j < kTJ; ++j) {
+      if (BITS == 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(as + av[h ^ (j & 1)][e] + j * 32 * T::kARow);
+        f.a[j][0] = v.x; f.a[j][1] = v.y; f.a[j][2] = v.z; f.a[j][3] = v.w;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const uint4 v = *reinterpret_cast<const uint4*>(as + av[h][2 * e + q] + j * 32 * T::kARow);
+          f.a[j][4 * q] = v.x; f.a[j][4 * q + 1] = v.y; f.a[j][4 * q + 2] = v.z; f.a[j][4 * q + 3] = v.w;
         }
       }
+    }
+  };
+
+  v16i acc[kTI][kTJ];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const v4i aop = ks == 0 ? op_from_nibbles(wf[i].x, wf[i].y) : op_from_nibbles(wf[i].z, wf[i].w);
+  for (int i = 0; i < kTI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma(aop, bop[j], acc[i][j]);
+    for (int j = 0; j < kTJ; ++j) acc[i][j] = v16i{};
+
+  // Two 32-k MFMA steps from one chunk pair.
+  auto compute_pair = [&](const Frags& f) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      v4i aop[kTJ];
+#pragma unroll
+      for (int j = 0; j < kTJ; ++j) {
+        if (BITS == 4) aop[j] = op_from_nibbles(f.a[j][2 * kk], f.a[j][2 * kk + 1]);
+        else aop[j] = op_from_bytes(f.a[j][4 * kk], f.a[j][4 * kk + 1], f.a[j][4 * kk + 2], f.a[j][4 * kk + 3]);
+      }
+#pragma unroll
+      for (int i = 0; i < kTI; ++i) {
+        const v4i wop = op_from_nibbles(f.w[i][2 * kk], f.w[i][2 * kk + 1]);
+#pragma unroll
+        for (int j = 0; j < kTJ; ++j) acc[i][j] = mfma32(wop, aop[j], acc[i][j]);
       }
     }
-    if (s + 1 < steps) sstore(buf ^ 1);
-    __syncthreads();
+  };
+
+  // Stage s: wait until it has landed (it is the only one in flight); the
+  // barrier also guarantees every wavefront is done with stage s-1, whose
+  // buffer the prefetch of stage s+1 refills.
+  Frags fa, fb;
+  auto begin_stage = [&](int s) __attribute__((always_inline)) -> const uint8_t* {
+    wait_vmcnt<0>();
+    lds_barrier();
+    if (s + 1 < nst) issue(s + 1, (s + 1) & 1);
+    return smem + (s & 1) * T::kStage;
+  };
+  issue(0, 0);
+  // The loop body is branch-free; the last stage (possibly holding only
+  // 128 k) is peeled off.
+  for (int s = 0; s < nst - 1; ++s) {
+    const uint8_t* buf = begin_stage(s);
+    read_pair(buf, 0, 0, fa);
+    read_pair(buf, 0, 1, fb);
+    compute_pair(fa);
+    read_pair(buf, 1, 0, fa);
+    compute_pair(fb);
+    read_pair(buf, 1, 1, fb);
+    compute_pair(fa);
+    compute_pair(fb);
+  }
+  {
+    const uint8_t* buf = begin_stage(nst - 1);
+    read_pair(buf, 0, 0, fa);
+    read_pair(buf, 0, 1, fb);
+    compute_pair(fa);
+    if (!half_tail) {
+      read_pair(buf, 1, 0, fa);
+      compute_pair(fb);
+      read_pair(buf, 1, 1, fb);
+      compute_pair(fa);
+      compute_pair(fb);
+    } else {
+      compute_pair(fb);
+    }
   }
 
-  // Epilogue: lane holds rows n = base + 4*fg + r (r = 0..3) of column m.
+  if (ACC_OUT) {
+    // Raw accumulators (verification path): direct 16-byte stores.
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int m = m0 + wm * 64 + j * 16 + fr;
-    if (m >= M) continue;
-    const float as = ACC_OUT ? 0.0f : a_scales[m];
+    for (int j = 0; j < kTJ; ++j) {
+      const int m = m0 + wm * kTJ * 32 + j * 32 + fr;
+      if (m >= M) continue;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int n = n0 + wn * 128 + i * 16 + fg * 4;
-      if (n >= N) continue;
-      const int c0 = unscale<BITS>(acc[i][j].x), c1 = unscale<BITS>(acc[i][j].y);
-      const int c2 = unscale<BITS>(acc[i][j].z), c3 = unscale<BITS>(acc[i][j].w);
-      if (ACC_OUT) {
-        *reinterpret_cast<int4*>(acc_out + (size_t)m * N + n) = make_int4(c0, c1, c2, c3);
-      } else {
-        const float4 wsv = *reinterpret_cast<const float4*>(w_scales + n);
-        const __half h0 = dequant(c0, as, wsv.x), h1 = dequant(c1, as, wsv.y);
-        const __half h2 = dequant(c2, as, wsv.z), h3 = dequant(c3, as, wsv.w);
+      for (int i = 0; i < kTI; ++i)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int n = n0 + wn * kTI * 32 + i * 32 + 8 * b + 4 * fg;
+          if (n >= N) continue;
+          *reinterpret_cast<int4*>(acc_out + (size_t)m * N + n) =
+              make_int4(unscale<BITS>(acc[i][j][4 * b]), unscale<BITS>(acc[i][j][4 * b + 1]),
+                        unscale<BITS>(acc[i][j][4 * b + 2]), unscale<BITS>(acc[i][j][4 * b + 3]));
+        }
+    }
+    return;
+  }
+
+  // Dequantize into an LDS copy of the fp16 tile (rows m, 256 n + padding),
+  // then write whole rows.  32 x 32 accumulator layout: lane l holds column
+  // m = l & 31 and, in registers 4b .. 4b+3, rows n = 8 b + 4 (l >> 5) + 0..3.
+  lds_barrier();   // every wavefront is done reading the last stage
+#pragma unroll
+  for (int j = 0; j < kTJ; ++j) {
+    const int ml = wm * kTJ * 32 + j * 32 + fr;
+    const float as = a_scales[min(m0 + ml, M - 1)];
+#pragma unroll
+    for (int i = 0; i < kTI; ++i) {
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int nl = wn * kTI * 32 + i * 32 + 8 * b + 4 * fg;
+        const float4 wsv = *reinterpret_cast<const float4*>(w_scales + min(n0 + nl, N - 4));
+        const __half h0 = dequant(unscale<BITS>(acc[i][j][4 * b]), as, wsv.x);
+        const __half h1 = dequant(unscale<BITS>(acc[i][j][4 * b + 1]), as, wsv.y);
+        const __half h2 = dequant(unscale<BITS>(acc[i][j][4 * b + 2]), as, wsv.z);
+        const __half h3 = dequant(unscale<BITS>(acc[i][j][4 * b + 3]), as, wsv.w);
         uint2 pk;
         pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
         pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
-        *reinterpret_cast<uint2*>(y + (size_t)m * N + n) = pk;
+        *reinterpret_cast<uint2*>(smem + ml * T::kOutStride + nl * 2) = pk;
       }
     }
+  }
+  lds_barrier();
+  // 32 threads per 512-byte output row, 8 rows per pass.
+  const int cc = t & 31;
+  for (int ml = t >> 5; ml < kBM; ml += kThreads / 32) {
+    const int m = m0 + ml, n = n0 + cc * 8;
+    if (m >= M || n >= N) continue;
+    const uint4 v = *reinterpret_cast<const uint4*>(smem + ml * T::kOutStride + cc * 16);
+    *reinterpret_cast<uint4*>(y + (size_t)m * N + n) = v;
   }
 }
 
