@@ -142,11 +142,16 @@ struct Tile {
   static constexpr int kARow = BITS == 4 ? kBK / 2 : kBK;      // 128 or 256 B
   static constexpr int kW = kBN * kWRow;                       // 32 KiB
   static constexpr int kA = kBM * kARow;                       // 16 or 32 KiB
-  static constexpr int kStage = kW + kA;
+  static constexpr int kStage = kW + kA;                       // 48 or 64 KiB
+  // Load buffers in the ring: as many as fit in 160 KiB (3 or 2), i.e. loads
+  // are issued 2 (or 1) stages ahead of their use.
+  static constexpr int kBufs = (160 * 1024) / kStage < 3 ? 2 : 3;
+  static constexpr int kLds = kBufs * kStage;
   static constexpr int kWLoads = kW / 1024 / kWaves;           // per wavefront
   static constexpr int kALoads = kA / 1024 / kWaves;
+  static constexpr int kLoads = kWLoads + kALoads;
   static constexpr int kOutStride = kBN * 2 + 16;              // fp16 output row in LDS
-  static_assert(kBM * kOutStride <= 2 * kStage, "output staging must fit the ring");
+  static_assert(kBM * kOutStride <= kLds, "output staging must fit the ring");
 };
 
 template <int BITS, bool ACC_OUT>
@@ -155,7 +160,7 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
               const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
               int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
   using T = Tile<BITS>;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * T::kStage];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[T::kLds];
 
   const int tiles_m = (M + kBM - 1) / kBM;
   const int tiles_n = N / kBN + (N % kBN ? 1 : 0);
@@ -275,6 +280,7 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
     uint32_t w[kTI][4];
     uint32_t a[kTJ][kAD];
   };
+  using WFrags = Frags;
   auto read_pair = [&](const uint8_t* buf, int h, int e, Frags& f) __attribute__((always_inline)) {
     const uint8_t* ws = buf;
     const uint8_t* as = buf + T::kW;
@@ -323,17 +329,26 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
     }
   };
 
-  // Stage s: wait until it has landed (it is the only one in flight); the
-  // barrier also guarantees every wavefront is done with stage s-1, whose
-  // buffer the prefetch of stage s+1 refills.
-  Frags fa, fb;
+  // Ring of kBufs load buffers, loads issued kBufs-1 stages ahead.  Every
+  // iteration issues exactly one stage (past the end the last stage again,
+  // L2-resident, into a buffer nobody reads any more), so the number of load
+  // instructions in flight is uniform: stage s has landed once only the
+  // kBufs-2 stages after it are outstanding.  The barrier also guarantees
+  // every wavefront is done with stage s-1, whose buffer the issue refills.
+  constexpr int kB = T::kBufs;
+  WFrags fa, fb;
+  int cur = 0;   // buffer of stage s
   auto begin_stage = [&](int s) __attribute__((always_inline)) -> const uint8_t* {
-    wait_vmcnt<0>();
+    wait_vmcnt<(kB - 2) * T::kLoads>();
     lds_barrier();
-    if (s + 1 < nst) issue(s + 1, (s + 1) & 1);
-    return smem + (s & 1) * T::kStage;
+    const int nb = cur == 0 ? kB - 1 : cur - 1;   // (s + kB - 1) % kB
+    issue(min(s + kB - 1, nst - 1), nb);
+    const uint8_t* buf = smem + cur * T::kStage;
+    cur = cur + 1 == kB ? 0 : cur + 1;
+    return buf;
   };
-  issue(0, 0);
+#pragma unroll
+  for (int st = 0; st < kB - 1; ++st) issue(min(st, nst - 1), st);
   // The loop body is branch-free; the last stage (possibly holding only
   // 128 k) is peeled off.
   for (int s = 0; s < nst - 1; ++s) {
@@ -362,6 +377,7 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
       compute_pair(fb);
     }
   }
+  wait_vmcnt<0>();   // the re-issued tail loads must land before LDS is reused
 
   if (ACC_OUT) {
     // Raw accumulators (verification path): direct 16-byte stores.
