@@ -37,11 +37,74 @@ def parse():
     p.add_argument("--copies", type=int, default=12,
                    help="distinct activation/weight copies cycled per step")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=24,
+    p.add_argument("--cpu-rows", type=int, default=160,
                    help="token rows of the workload the CPU oracle is timed on")
     p.add_argument("--extended", action="store_true",
                    help="also time the decode shapes and the 28 x 512 rotation")
+    p.add_argument("--only", choices=["rq4", "gemm4", "rq8", "gemm8", "copy"],
+                   help="run one kernel of the step --steps times (for counter runs) "
+                        "or, with copy, a plain device copy of 256 MiB (counter calibration)")
     return p.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_prefill_a4_llama2_7b_qkv.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_12487_amd", "csrc", "qgemm.hip")
+
+
+def source_digest(path):
+    import hashlib
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the A4 GEMM from the committed counter summary,
+    or None when it is missing or was taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != source_digest(KERNEL_SOURCE):
+        return None
+    try:
+        return int(float(kv["hbm_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def run_only(torch, dptq, cfg, args):
+    """One kernel, repeated; nothing timed.  Used under rocprofv3 --pmc."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    if args.only == "copy":
+        n = 256 << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n}))
+        return
+    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
+    rng = np.random.default_rng(cfg["seed"])
+    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
+    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
+    wp, ws = dptq.prepare_weights(w, h)
+    del w
+    bits = 4 if args.only.endswith("4") else 8
+    codes, scales = dptq.rotate_quant(x, h, bits)
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        if args.only.startswith("rq"):
+            dptq.rotate_quant(x, h, bits, codes, scales)
+        else:
+            dptq.qlinear(codes, scales, bits, wp, ws, y)
+    torch.cuda.synchronize()
+    print(json.dumps({"only": args.only, "launches": args.steps}))
 
 
 def _events(torch, n):
@@ -190,6 +253,9 @@ def main():
     dptq.lib()
     cfg = workloads.CONFIGS["llama2_7b_qkv"]
     M, K, N = cfg["M"], cfg["K"], cfg["N"]
+    if args.only:
+        run_only(torch, dptq, cfg, args)
+        return
 
     wall, per, seq = time_layer(torch, dptq, cfg, args)
     ops_gemm = 2.0 * M * N * K
@@ -211,7 +277,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "qgemm_prefill<4>",
                      "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic()},
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
         "rotate_quant_a4_GBs": round(k1_bytes / (per[f"rotate_quant_a{seq[0]}"] * 1e-3) / 1e9, 1),
     }

@@ -77,27 +77,26 @@ __device__ __forceinline__ __half dequant(int acc, float as, float ws) {
 }
 
 // ---------------------------------------------------------------------------
-// Prefill: 256 (n) x 128 (m) output tiles on 8 wavefronts (two per SIMD) of
-// 64 (n) x 64 (m), each a 2 x 2 grid of 32 x 32 x 32 int8 MFMAs.  K is consumed in stages of
-// 256 (128-byte row slices for 4-bit operands, so every global request is a
-// full cache line) through two LDS buffers filled by direct global->LDS
-// 16-byte loads; the next stage streams in while the current one is
-// computed.  The fp16 tile is staged through LDS so that the output rows are
-// written with coalesced 16-byte stores.
+// Prefill.  An output tile of BN (n) x BM (m) is computed by WN x WM
+// wavefronts, each owning a TI x TJ grid of 32 x 32 x 32 int8 MFMAs.  K is
+// consumed in stages of 256 (128-byte row slices for 4-bit operands, so every
+// global request is a full cache line) through a ring of LDS buffers filled
+// by direct global->LDS 16-byte loads issued ahead of use.  The fp16 tile is
+// staged through LDS so output rows are written with coalesced stores.
+//
+// The instantiated shape is 256 x 128 on eight wavefronts of 64 x 64, two
+// per SIMD: one wavefront's unpack and LDS reads co-execute with the other's
+// MFMAs.  (A 192 x 256 tile on four wavefronts of 96 x 128 moves fewer LDS
+// bytes per MFMA but, at one wavefront per SIMD, measured slower.)
 // ---------------------------------------------------------------------------
-constexpr int kBN = 256, kBM = 128, kBK = 256;
-// Wavefront grid and per-wavefront MFMA tiles (32 x 32 each).
-constexpr int kWN = 4, kWM = 2;              // wavefronts along n and m
-constexpr int kTI = kBN / kWN / 32;          // 32-row n tiles per wavefront (2)
-constexpr int kTJ = kBM / kWM / 32;          // 32-row m tiles per wavefront (2)
-constexpr int kWaves = kWN * kWM, kThreads = kWaves * 64;
+constexpr int kBK = 256;
 
 typedef __attribute__((address_space(3))) uint8_t* lds_ptr;
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 // One wavefront-wide 16-byte-per-lane direct load from global memory into LDS
 // at byte offset lds_off (+ 16 * lane).  Issued as asm so that the compiler's
-// conservative wait (it cannot tell the two buffers apart) does not drain
+// conservative wait (it cannot tell the ring buffers apart) does not drain
 // the loads before every LDS read; completion is tracked with wait_vmcnt.
 // Address = wavefront-uniform base + 32-bit per-lane offset.
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_off) {
@@ -136,34 +135,43 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
   return x * per + (x < rem ? x : rem) + idx;
 }
 
-template <int BITS>
-struct Tile {
+template <int BITS, int BN, int BM, int WN, int WM>
+struct Cfg {
+  static constexpr int kBits = BITS, kBN = BN, kBM = BM, kWN = WN, kWM = WM;
+  static constexpr int kWaves = WN * WM, kThreads = kWaves * 64;
+  static constexpr int kTI = BN / WN / 32, kTJ = BM / WM / 32;
   static constexpr int kWRow = kBK / 2;                        // 128 B
   static constexpr int kARow = BITS == 4 ? kBK / 2 : kBK;      // 128 or 256 B
-  static constexpr int kW = kBN * kWRow;                       // 32 KiB
-  static constexpr int kA = kBM * kARow;                       // 16 or 32 KiB
-  static constexpr int kStage = kW + kA;                       // 48 or 64 KiB
-  // Load buffers in the ring: as many as fit in 160 KiB (3 or 2), i.e. loads
-  // are issued 2 (or 1) stages ahead of their use.
-  static constexpr int kBufs = (160 * 1024) / kStage < 3 ? 2 : 3;
-  static constexpr int kLds = kBufs * kStage;
+  static constexpr int kW = BN * kWRow;
+  static constexpr int kA = BM * kARow;
+  static constexpr int kStage = kW + kA;
+  // Load buffers: as many as fit in 160 KiB, at most 3 (loads issued up to
+  // two stages ahead).
+  static constexpr int kBufs = (160 * 1024) / kStage >= 3 ? 3 : 2;
+  static constexpr int kOutStride = BN * 2 + 16;               // fp16 output row in LDS
+  static constexpr int kLds = kBufs * kStage > BM * kOutStride ? kBufs * kStage : BM * kOutStride;
   static constexpr int kWLoads = kW / 1024 / kWaves;           // per wavefront
   static constexpr int kALoads = kA / 1024 / kWaves;
   static constexpr int kLoads = kWLoads + kALoads;
-  static constexpr int kOutStride = kBN * 2 + 16;              // fp16 output row in LDS
-  static_assert(kBM * kOutStride <= kLds, "output staging must fit the ring");
+  static_assert(kW % (1024 * kWaves) == 0 && kA % (1024 * kWaves) == 0, "load split");
+  static_assert(kWaves == 4 || kWaves == 8, "load swizzle assumes 4 or 8 wavefronts");
+  static_assert(kLds <= 160 * 1024, "LDS budget");
+  static_assert(BN % (WN * 32) == 0 && BM % (WM * 32) == 0, "wave tiles");
 };
 
-template <int BITS, bool ACC_OUT>
-__global__ void __launch_bounds__(kThreads)
+template <int BITS> using PrefillCfg = Cfg<BITS, 256, 128, 4, 2>;
+
+template <class C, bool ACC_OUT>
+__global__ void __launch_bounds__(C::kThreads)
 qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
               const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
               int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
-  using T = Tile<BITS>;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[T::kLds];
+  constexpr int BITS = C::kBits, kBN = C::kBN, kBM = C::kBM, kWN = C::kWN;
+  constexpr int kTI = C::kTI, kTJ = C::kTJ, kWaves = C::kWaves, kThreads = C::kThreads;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[C::kLds];
 
   const int tiles_m = (M + kBM - 1) / kBM;
-  const int tiles_n = N / kBN + (N % kBN ? 1 : 0);
+  const int tiles_n = (N + kBN - 1) / kBN;
   const int logical = xcd_remap(blockIdx.x, tiles_m * tiles_n);
   const int tm = logical % tiles_m, tn = logical / tiles_m;
   const int m0 = tm * kBM, n0 = tn * kBN;
@@ -178,44 +186,45 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
   // Direct loads.  One load instruction fills 1 KiB of LDS: 8 rows of 128 B
   // (4-bit operands) or 4 rows of 256 B (8-bit activations); lane l writes
   // physical chunk p of its row, which holds logical chunk p ^ swizzle(row).
-  // Load i of wavefront w fills LDS block i * kWaves + w: rows
-  // (i * kWaves + w) * 8 + (l >> 3) (resp. * 4 + (l >> 4)).  With 8
-  // wavefronts the swizzle of those rows does not depend on i, so the row
-  // part of the address is a wavefront-uniform base and the lane part a single
-  // offset.  Tiles that overhang the matrix clamp rows to the last one, and a
-  // half tail stage (K % 256 == 128) maps chunks past K onto their first-half
-  // twins; both only feed results that are never stored.
-  static_assert(kWaves == 8, "load swizzle assumes 8 wavefronts");
+  // Load i of wavefront w fills LDS block j = i * kWaves + w, rows j * 8 +
+  // (l >> 3) (resp. j * 4 + (l >> 4)).  The swizzle's row term is (j & 7)
+  // (resp. 4 (j & 3) + (l >> 4)), which depends on i at most through i & 1,
+  // so the row part of the address is a wavefront-uniform base and the lane
+  // part one of two offsets.  Tiles that overhang the matrix clamp rows to
+  // the last one, and a half tail stage (K % 256 == 128) maps chunks past K
+  // onto their first-half twins; both only feed results that are never stored.
   constexpr int kARows = BITS == 4 ? 8 : 4;   // rows per A load instruction
   const bool w_full = n0 + kBN <= N;
   const bool a_full = m0 + kBM <= M;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);   // known wavefront-uniform
-  uint32_t wlane, alane;
-  {
-    const int rl = lane >> 3;                       // swz8(r) = (rl ^ wave) & 7
-    const int c = ((lane & 7) ^ rl ^ wave) & 7;
-    wlane = (uint32_t)(rl * wrow + c * 16);
+  uint32_t wlane[2], alane[2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    const int rl = lane >> 3;
+    const int jlow = (x * kWaves + wave) & 7;        // (i * kWaves + w) & 7 for i & 1 == x
+    const int c = ((lane & 7) ^ rl ^ jlow) & 7;
+    wlane[x] = (uint32_t)(rl * wrow + c * 16);
     if (BITS == 4) {
-      alane = (uint32_t)(rl * arow + c * 16);
+      alane[x] = (uint32_t)(rl * arow + c * 16);
     } else {
-      const int r16 = (wave & 3) * 4 + (lane >> 4);   // swz16(r) = r & 15 = r16
-      alane = (uint32_t)((lane >> 4) * arow + ((lane & 15) ^ r16) * 16);
+      const int r16 = ((x * kWaves + wave) & 3) * 4 + (lane >> 4);
+      alane[x] = (uint32_t)((lane >> 4) * arow + ((lane & 15) ^ r16) * 16);
     }
   }
   const uint32_t smem_base = (uint32_t)(uintptr_t)(lds_ptr)smem;
   const uint32_t wave_off = (uint32_t)wave_u * 1024;
   auto issue = [&](int st, int buf) __attribute__((always_inline)) {
-    const uint32_t base = smem_base + buf * T::kStage + wave_off;
+    const uint32_t base = smem_base + buf * C::kStage + wave_off;
     const bool tail = half_tail && st == nst - 1;
-    const uint8_t* wt = w_packed + (size_t)n0 * wrow + (size_t)st * T::kWRow;   // uniform
-    const uint8_t* at = a_codes + (size_t)m0 * arow + (size_t)st * T::kARow;    // uniform
+    const uint8_t* wt = w_packed + (size_t)n0 * wrow + (size_t)st * C::kWRow;   // uniform
+    const uint8_t* at = a_codes + (size_t)m0 * arow + (size_t)st * C::kARow;    // uniform
     if (w_full && !tail) {
 #pragma unroll
-      for (int i = 0; i < T::kWLoads; ++i)
-        dma16(wt + (size_t)((i * kWaves + wave_u) * 8) * wrow, wlane, base + i * kWaves * 1024);
+      for (int i = 0; i < C::kWLoads; ++i)
+        dma16(wt + (size_t)((i * kWaves + wave_u) * 8) * wrow, wlane[i & 1], base + i * kWaves * 1024);
     } else {
 #pragma unroll
-      for (int i = 0; i < T::kWLoads; ++i) {
+      for (int i = 0; i < C::kWLoads; ++i) {
         const int r = (i * kWaves + wave) * 8 + (lane >> 3);
         int c = (lane & 7) ^ swz8(r);
         if (tail) c &= 3;
@@ -225,12 +234,12 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
     }
     if (a_full && !tail) {
 #pragma unroll
-      for (int i = 0; i < T::kALoads; ++i)
-        dma16(at + (size_t)((i * kWaves + wave_u) * kARows) * arow, alane,
-              base + T::kW + i * kWaves * 1024);
+      for (int i = 0; i < C::kALoads; ++i)
+        dma16(at + (size_t)((i * kWaves + wave_u) * kARows) * arow, alane[i & 1],
+              base + C::kW + i * kWaves * 1024);
     } else {
 #pragma unroll
-      for (int i = 0; i < T::kALoads; ++i) {
+      for (int i = 0; i < C::kALoads; ++i) {
         int r, c;
         if (BITS == 4) {
           r = (i * kWaves + wave) * 8 + (lane >> 3);
@@ -242,62 +251,66 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
           if (tail) c &= 7;
         }
         const int rc = min(r, M - 1 - m0);
-        dma16(at, (uint32_t)(rc * arow + c * 16), base + T::kW + i * kWaves * 1024);
+        dma16(at, (uint32_t)(rc * arow + c * 16), base + C::kW + i * kWaves * 1024);
       }
     }
   };
 
   // Fragment addresses.  In half h (128 k) of a stage, lane l reads row l & 31
-  // of its 32-row tile, k range [128 h + 64 g, +64), g = l >> 5: two 16-byte
+  // of its 32-row tiles, k range [128 h + 64 g, +64), g = l >> 5: two 16-byte
   // chunks of a 4-bit row, four of an 8-bit row.  The tile index enters as an
-  // immediate offset; for 4-bit rows the swizzle of tile i's row differs from
-  // tile 0's by 4 (i & 1), so only [h ^ (i & 1)][e] variants are needed.
+  // immediate offset.  For 4-bit rows the swizzle's row term for tile i is
+  // 4 ((t0 + i) & 1) ^ s0, t0 = the wavefront's first tile index, so the
+  // precomputed variants are indexed by h ^ (i & 1) with t0's parity folded in.
   const int fr = lane & 31, fg = lane >> 5;
   const int s0 = (fr & 7) ^ (fr >> 3);
+  const int pw = (wn * kTI) & 1, pa = (wm * kTJ) & 1;
   uint32_t wv[2][2];
   uint32_t av[2][4];
 #pragma unroll
-  for (int x = 0; x < 2; ++x)
+  for (int z = 0; z < 2; ++z)
 #pragma unroll
     for (int e = 0; e < 2; ++e)
-      wv[x][e] = (uint32_t)((wn * kTI * 32 + fr) * T::kWRow + (((2 * fg) ^ s0 ^ (4 * x + e)) & 7) * 16);
+      wv[z][e] = (uint32_t)((wn * kTI * 32 + fr) * C::kWRow +
+                            (((2 * fg) ^ s0 ^ (4 * (z ^ pw) + e)) & 7) * 16);
 #pragma unroll
-  for (int x = 0; x < 2; ++x)
+  for (int z = 0; z < 2; ++z)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       if (BITS == 4)
-        av[x][e] = e < 2 ? (uint32_t)((wm * kTJ * 32 + fr) * T::kARow + (((2 * fg) ^ s0 ^ (4 * x + e)) & 7) * 16) : 0u;
+        av[z][e] = e < 2 ? (uint32_t)((wm * kTJ * 32 + fr) * C::kARow +
+                                      (((2 * fg) ^ s0 ^ (4 * (z ^ pa) + e)) & 7) * 16)
+                         : 0u;
       else
-        av[x][e] = (uint32_t)((wm * kTJ * 32 + fr) * T::kARow + (((8 * x + 4 * fg + e) ^ (fr & 15)) & 15) * 16);
+        av[z][e] = (uint32_t)((wm * kTJ * 32 + fr) * C::kARow + (((8 * z + 4 * fg + e) ^ (fr & 15)) & 15) * 16);
     }
 
   // A stage is consumed as four chunk pairs p = 2 h + e: the 16-byte chunk e
   // of half h of every fragment row, i.e. two 32-k MFMA steps.  The packed
-  // fragments of pair p+1 are read from LDS while pair p is unpacked and
-  // multiplied.
+  // fragments of the next pair are read from LDS while the current one is
+  // unpacked and multiplied.
   constexpr int kAD = BITS == 4 ? 4 : 8;
   struct Frags {
     uint32_t w[kTI][4];
     uint32_t a[kTJ][kAD];
   };
-  using WFrags = Frags;
   auto read_pair = [&](const uint8_t* buf, int h, int e, Frags& f) __attribute__((always_inline)) {
     const uint8_t* ws = buf;
-    const uint8_t* as = buf + T::kW;
+    const uint8_t* as = buf + C::kW;
 #pragma unroll
     for (int i = 0; i < kTI; ++i) {
-      const uint4 v = *reinterpret_cast<const uint4*>(ws + wv[h ^ (i & 1)][e] + i * 32 * T::kWRow);
+      const uint4 v = *reinterpret_cast<const uint4*>(ws + wv[h ^ (i & 1)][e] + i * 32 * C::kWRow);
       f.w[i][0] = v.x; f.w[i][1] = v.y; f.w[i][2] = v.z; f.w[i][3] = v.w;
     }
 #pragma unroll
     for (int j = 0; j < kTJ; ++j) {
       if (BITS == 4) {
-        const uint4 v = *reinterpret_cast<const uint4*>(as + av[h ^ (j & 1)][e] + j * 32 * T::kARow);
+        const uint4 v = *reinterpret_cast<const uint4*>(as + av[h ^ (j & 1)][e] + j * 32 * C::kARow);
         f.a[j][0] = v.x; f.a[j][1] = v.y; f.a[j][2] = v.z; f.a[j][3] = v.w;
       } else {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-          const uint4 v = *reinterpret_cast<const uint4*>(as + av[h][2 * e + q] + j * 32 * T::kARow);
+          const uint4 v = *reinterpret_cast<const uint4*>(as + av[h][2 * e + q] + j * 32 * C::kARow);
           f.a[j][4 * q] = v.x; f.a[j][4 * q + 1] = v.y; f.a[j][4 * q + 2] = v.z; f.a[j][4 * q + 3] = v.w;
         }
       }
@@ -335,15 +348,15 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
   // instructions in flight is uniform: stage s has landed once only the
   // kBufs-2 stages after it are outstanding.  The barrier also guarantees
   // every wavefront is done with stage s-1, whose buffer the issue refills.
-  constexpr int kB = T::kBufs;
-  WFrags fa, fb;
+  constexpr int kB = C::kBufs;
+  Frags fa, fb;
   int cur = 0;   // buffer of stage s
   auto begin_stage = [&](int s) __attribute__((always_inline)) -> const uint8_t* {
-    wait_vmcnt<(kB - 2) * T::kLoads>();
+    wait_vmcnt<(kB - 2) * C::kLoads>();
     lds_barrier();
     const int nb = cur == 0 ? kB - 1 : cur - 1;   // (s + kB - 1) % kB
     issue(min(s + kB - 1, nst - 1), nb);
-    const uint8_t* buf = smem + cur * T::kStage;
+    const uint8_t* buf = smem + cur * C::kStage;
     cur = cur + 1 == kB ? 0 : cur + 1;
     return buf;
   };
@@ -399,7 +412,7 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
     return;
   }
 
-  // Dequantize into an LDS copy of the fp16 tile (rows m, 256 n + padding),
+  // Dequantize into an LDS copy of the fp16 tile (rows m, BN n + padding),
   // then write whole rows.  32 x 32 accumulator layout: lane l holds column
   // m = l & 31 and, in registers 4b .. 4b+3, rows n = 8 b + 4 (l >> 5) + 0..3.
   lds_barrier();   // every wavefront is done reading the last stage
@@ -420,17 +433,18 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
         uint2 pk;
         pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
         pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
-        *reinterpret_cast<uint2*>(smem + ml * T::kOutStride + nl * 2) = pk;
+        *reinterpret_cast<uint2*>(smem + ml * C::kOutStride + nl * 2) = pk;
       }
     }
   }
   lds_barrier();
-  // 32 threads per 512-byte output row, 8 rows per pass.
-  const int cc = t & 31;
-  for (int ml = t >> 5; ml < kBM; ml += kThreads / 32) {
+  // Rows of BN halves = BN / 8 16-byte chunks.
+  constexpr int kRowChunks = kBN / 8;
+  for (int idx = t; idx < kBM * kRowChunks; idx += kThreads) {
+    const int ml = idx / kRowChunks, cc = idx - ml * kRowChunks;
     const int m = m0 + ml, n = n0 + cc * 8;
     if (m >= M || n >= N) continue;
-    const uint4 v = *reinterpret_cast<const uint4*>(smem + ml * T::kOutStride + cc * 16);
+    const uint4 v = *reinterpret_cast<const uint4*>(smem + ml * C::kOutStride + cc * 16);
     *reinterpret_cast<uint4*>(y + (size_t)m * N + n) = v;
   }
 }
@@ -520,6 +534,14 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
   }
 }
 
+template <class C, bool ACC_OUT>
+void launch_prefill(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
+                    const float* ws, int64_t N, __half* y, int32_t* acc, hipStream_t stream) {
+  const int64_t tiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
+  hipLaunchKernelGGL((qgemm_prefill<C, ACC_OUT>), dim3((unsigned)tiles), dim3(C::kThreads), 0,
+                     stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+}
+
 template <int BITS, bool ACC_OUT>
 hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
                     const uint8_t* w, const float* ws, int64_t N, __half* y,
@@ -529,9 +551,7 @@ hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
     hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT>), dim3((unsigned)(N / 16)),
                        dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
   } else {
-    const int64_t tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-    hipLaunchKernelGGL((qgemm_prefill<BITS, ACC_OUT>), dim3((unsigned)tiles), dim3(kThreads), 0,
-                       stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+    launch_prefill<PrefillCfg<BITS>, ACC_OUT>(a, as, M, K, w, ws, N, y, acc, stream);
   }
   return hipGetLastError();
 }

@@ -1,0 +1,118 @@
+"""Turn rocprofv3 CSV output into the short text summaries kept under profiles/.
+
+    python -m paper_2606_12487_amd.rocprof_summary stats STATS_CSV [--title T] [--command C]
+    python -m paper_2606_12487_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV \
+        COPY_FETCH_CSV COPY_WRITE_CSV --kernel SUBSTR --source FILE \
+        --algorithmic-bytes B [--title T] [--command C]
+
+`stats` reads rocprofv3's kernel statistics (--kernel-trace --stats
+--output-format csv) and prints one row per kernel.  `traffic` reads two
+counter runs of a kernel (FETCH_SIZE, WRITE_SIZE: KiB per dispatch) and the
+same counters for a device copy of 256 MiB, scales the kernel's figures by
+known-bytes / counted-bytes of the copy, and prints HBM bytes per launch
+together with the kernel source digest they belong to.
+"""
+
+import argparse
+import csv
+import hashlib
+import statistics
+import sys
+
+COPY_BYTES = 256 << 20
+
+
+def _rows(path):
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def stats(path, title, command):
+    rows = _rows(path)
+    out = [f"# {title}" if title else "# rocprofv3 kernel statistics"]
+    if command:
+        out.append(f"# command: {command}")
+    out.append(f"# source: {path.split('/')[-1]}")
+    out.append("kernel | calls | total_us | average_us | min_us | max_us | percent")
+    for r in rows:
+        name = r.get("Name", "?")
+        calls = int(float(r.get("Calls", 0)))
+        tot = float(r.get("TotalDurationNs", 0)) / 1e3
+        avg = float(r.get("AverageNs", 0)) / 1e3
+        mn = float(r.get("MinNs", 0)) / 1e3
+        mx = float(r.get("MaxNs", 0)) / 1e3
+        pct = float(r.get("Percentage", 0))
+        out.append(f"{name} | {calls} | {tot:.1f} | {avg:.2f} | {mn:.2f} | {mx:.2f} | {pct:.1f}")
+    return "\n".join(out)
+
+
+def _counter(path, counter, kernel):
+    vals = [float(r["Counter_Value"]) for r in _rows(path)
+            if r["Counter_Name"] == counter and kernel in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"no {counter} rows for kernels matching {kernel!r} in {path}")
+    return statistics.median(vals), len(vals)
+
+
+def traffic(a, title, command):
+    fetch, nf = _counter(a.fetch_csv, "FETCH_SIZE", a.kernel)
+    write, nw = _counter(a.write_csv, "WRITE_SIZE", a.kernel)
+    cfetch, _ = _counter(a.copy_fetch_csv, "FETCH_SIZE", a.copy_kernel)
+    cwrite, _ = _counter(a.copy_write_csv, "WRITE_SIZE", a.copy_kernel)
+    fscale = COPY_BYTES / (cfetch * 1024.0)
+    wscale = COPY_BYTES / (cwrite * 1024.0)
+    fb = fetch * 1024.0 * fscale
+    wb = write * 1024.0 * wscale
+    digest = hashlib.sha256(open(a.source, "rb").read()).hexdigest()[:16]
+    out = [f"# {title}" if title else "# HBM traffic per launch"]
+    if command:
+        for c in command.split(" ;; "):
+            out.append(f"# command: {c}")
+    out += [
+        f"kernel: {a.kernel}",
+        f"source: {a.source.split('/')[-1]}",
+        f"source_sha256_16: {digest}",
+        f"dispatches_fetch: {nf}",
+        f"dispatches_write: {nw}",
+        f"fetch_kib_per_launch: {fetch:.1f}",
+        f"write_kib_per_launch: {write:.1f}",
+        f"copy_fetch_kib: {cfetch:.1f}",
+        f"copy_write_kib: {cwrite:.1f}",
+        f"fetch_scale: {fscale:.4f}",
+        f"write_scale: {wscale:.4f}",
+        f"hbm_read_bytes_per_launch: {fb:.0f}",
+        f"hbm_write_bytes_per_launch: {wb:.0f}",
+        f"hbm_bytes_per_launch: {fb + wb:.0f}",
+        f"algorithmic_bytes_per_launch: {a.algorithmic_bytes}",
+        f"traffic_over_algorithmic: {(fb + wb) / a.algorithmic_bytes:.3f}",
+    ]
+    return "\n".join(out)
+
+
+def main(argv=None):
+    p = argparse.ArgumentParser()
+    sub = p.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("--title", default="")
+    s.add_argument("--command", default="")
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch_csv")
+    t.add_argument("write_csv")
+    t.add_argument("copy_fetch_csv")
+    t.add_argument("copy_write_csv")
+    t.add_argument("--kernel", required=True)
+    t.add_argument("--copy-kernel", default="")
+    t.add_argument("--source", required=True)
+    t.add_argument("--algorithmic-bytes", type=int, required=True)
+    t.add_argument("--title", default="")
+    t.add_argument("--command", default="")
+    a = p.parse_args(argv)
+    if a.cmd == "stats":
+        print(stats(a.csv, a.title, a.command))
+    else:
+        print(traffic(a, a.title, a.command))
+
+
+if __name__ == "__main__":
+    sys.exit(main())
