@@ -93,7 +93,8 @@ int dptq_rotate_quant(const void* x, int64_t M, int64_t K, int32_t had_size,
  *   codes    device, activation codes in the dptq_rotate_quant layout
  *   a_scales device, float [M]
  *   M        tokens >= 0; M <= 16 runs the weight-streaming decode kernel,
- *            larger M the MFMA tile kernel (same results bit for bit)
+ *            larger M one of two MFMA tile kernels, whichever the shape
+ *            keeps busier (same results bit for bit; see dptq_qlinear_kernel)
  *   K        multiple of 128, 128 <= K <= DPTQ_MAX_K
  *   bits     activation bits, 4 or 8
  *   w_packed device, uint8 [N, K/2]: 4-bit weight codes, same nibble layout as
@@ -114,6 +115,28 @@ int dptq_qlinear(const void* codes, const float* a_scales, int64_t M, int64_t K,
 int dptq_qlinear_acc(const void* codes, int64_t M, int64_t K, int32_t bits,
                      const uint8_t* w_packed, int64_t N, int32_t* acc,
                      void* stream);
+
+/* GEMM kernels of dptq_qlinear_kernel.  All return the same bits. */
+typedef enum {
+  DPTQ_GEMM_AUTO = 0,          /* the choice dptq_qlinear makes */
+  DPTQ_GEMM_DECODE = 1,        /* weight streaming; M <= 16 */
+  DPTQ_GEMM_TILE_256X128 = 2,  /* 256 (n) x 128 (m) output tiles; any M */
+  DPTQ_GEMM_TILE_192X256 = 3   /* 192 (n) x 256 (m) tiles, persistent;
+                                  M >= 256, N >= 192, K >= 512 */
+} dptq_gemm_kernel;
+
+/*
+ * dptq_qlinear_kernel - dptq_qlinear (y != NULL; a_scales and w_scales
+ * required, acc NULL) or dptq_qlinear_acc (acc != NULL; scales ignored, y
+ * NULL) on a chosen kernel, for verification, benchmarks and tuning: every
+ * kernel returns the same bits and the choice only changes speed.  Same
+ * argument rules as dptq_qlinear; DPTQ_ERR_UNSUPPORTED when the shape is
+ * outside the kernel's range, DPTQ_ERR_INVALID_ARG for an unknown kernel or
+ * when not exactly one of y and acc is given.
+ */
+int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                        int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                        int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream);
 
 /*
  * dptq_layer_policy - phase-aware activation precision (host only).

@@ -15,7 +15,8 @@ import ctypes
 import os
 
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
-           "layer_policy", "prepare_weights", "version", "EXPORTED_FUNCTIONS"]
+           "layer_policy", "prepare_weights", "version", "EXPORTED_FUNCTIONS", "GEMM_AUTO",
+           "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libdptq.so"
@@ -23,8 +24,11 @@ _lib = None
 
 # Every function the C ABI exports (include/dptq.h).
 EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
-                      "dptq_qlinear", "dptq_qlinear_acc", "dptq_layer_policy",
-                      "dptq_prepare_weights")
+                      "dptq_qlinear", "dptq_qlinear_acc", "dptq_qlinear_kernel",
+                      "dptq_layer_policy", "dptq_prepare_weights")
+
+# GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
+GEMM_AUTO, GEMM_DECODE, GEMM_TILE_256X128, GEMM_TILE_192X256 = 0, 1, 2, 3
 
 
 class DptqError(RuntimeError):
@@ -58,6 +62,8 @@ def lib():
         L.dptq_qlinear.restype = ctypes.c_int
         L.dptq_qlinear_acc.argtypes = [vp, i64, i64, i32, vp, i64, vp, vp]
         L.dptq_qlinear_acc.restype = ctypes.c_int
+        L.dptq_qlinear_kernel.argtypes = [vp, vp, i64, i64, i32, vp, vp, i64, vp, vp, i32, vp]
+        L.dptq_qlinear_kernel.restype = ctypes.c_int
         L.dptq_layer_policy.argtypes = [i32, vp, vp]
         L.dptq_layer_policy.restype = ctypes.c_int
         L.dptq_prepare_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp]
@@ -150,8 +156,9 @@ def _gemm_args(codes, bits, w_packed):
     return M, K, N
 
 
-def qlinear(codes, a_scales, bits, w_packed, w_scales, y=None):
-    """y [M, N] fp16 = dequant(codes . w^T) with per-token x per-channel scales."""
+def qlinear(codes, a_scales, bits, w_packed, w_scales, y=None, kernel=GEMM_AUTO):
+    """y [M, N] fp16 = dequant(codes . w^T) with per-token x per-channel scales.
+    kernel: one of the GEMM_* kernels (default: the library's choice)."""
     torch = _torch()
     M, K, N = _gemm_args(codes, bits, w_packed)
     _require(a_scales, "a_scales", torch.float32, (M,))
@@ -159,20 +166,30 @@ def qlinear(codes, a_scales, bits, w_packed, w_scales, y=None):
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
     _require(y, "y", torch.float16, (M, N))
-    _check(lib().dptq_qlinear(_ptr(codes), _ptr(a_scales), M, K, int(bits), _ptr(w_packed),
-                              _ptr(w_scales), N, _ptr(y), _stream(codes)), "dptq_qlinear")
+    if kernel == GEMM_AUTO:
+        _check(lib().dptq_qlinear(_ptr(codes), _ptr(a_scales), M, K, int(bits), _ptr(w_packed),
+                                  _ptr(w_scales), N, _ptr(y), _stream(codes)), "dptq_qlinear")
+    else:
+        _check(lib().dptq_qlinear_kernel(_ptr(codes), _ptr(a_scales), M, K, int(bits),
+                                         _ptr(w_packed), _ptr(w_scales), N, _ptr(y), None,
+                                         int(kernel), _stream(codes)), "dptq_qlinear_kernel")
     return y
 
 
-def qlinear_acc(codes, bits, w_packed, acc=None):
+def qlinear_acc(codes, bits, w_packed, acc=None, kernel=GEMM_AUTO):
     """Raw int32 accumulators acc [M, N] = codes . w^T (exact)."""
     torch = _torch()
     M, K, N = _gemm_args(codes, bits, w_packed)
     if acc is None:
         acc = torch.empty((M, N), dtype=torch.int32, device=codes.device)
     _require(acc, "acc", torch.int32, (M, N))
-    _check(lib().dptq_qlinear_acc(_ptr(codes), M, K, int(bits), _ptr(w_packed), N, _ptr(acc),
-                                  _stream(codes)), "dptq_qlinear_acc")
+    if kernel == GEMM_AUTO:
+        _check(lib().dptq_qlinear_acc(_ptr(codes), M, K, int(bits), _ptr(w_packed), N, _ptr(acc),
+                                      _stream(codes)), "dptq_qlinear_acc")
+    else:
+        _check(lib().dptq_qlinear_kernel(_ptr(codes), None, M, K, int(bits), _ptr(w_packed), None,
+                                         N, None, _ptr(acc), int(kernel), _stream(codes)),
+               "dptq_qlinear_kernel")
     return acc
 
 

@@ -92,7 +92,7 @@ int dptq_qlinear(const void* codes, const float* a_scales, int64_t M, int64_t K,
       !aligned16(w_scales) || !aligned16(y))
     return DPTQ_ERR_INVALID_ARG;
   return from_hip(dptq::launch_qlinear(codes, a_scales, M, (int)K, bits, w_packed, w_scales, N,
-                                       y, nullptr, static_cast<hipStream_t>(stream)));
+                                       y, nullptr, dptq::kGemmAuto, static_cast<hipStream_t>(stream)));
 }
 
 int dptq_qlinear_acc(const void* codes, int64_t M, int64_t K, int32_t bits,
@@ -103,7 +103,29 @@ int dptq_qlinear_acc(const void* codes, int64_t M, int64_t K, int32_t bits,
   if (!codes || !w_packed || !acc) return DPTQ_ERR_INVALID_ARG;
   if (!aligned16(codes) || !aligned16(w_packed) || !aligned16(acc)) return DPTQ_ERR_INVALID_ARG;
   return from_hip(dptq::launch_qlinear(codes, nullptr, M, (int)K, bits, w_packed, nullptr, N,
-                                       nullptr, acc, static_cast<hipStream_t>(stream)));
+                                       nullptr, acc, dptq::kGemmAuto, static_cast<hipStream_t>(stream)));
+}
+
+int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                        int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                        int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream) {
+  int st = check_gemm_shape(M, K, bits, N);
+  if (st != DPTQ_OK) return st;
+  if (kernel < DPTQ_GEMM_AUTO || kernel > DPTQ_GEMM_TILE_192X256) return DPTQ_ERR_INVALID_ARG;
+  if ((y == nullptr) == (acc == nullptr)) return DPTQ_ERR_INVALID_ARG;
+  if (!dptq::gemm_kernel_fits(kernel, M, N, (int)K, bits)) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!codes || !w_packed) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(w_packed)) return DPTQ_ERR_INVALID_ARG;
+  if (y) {
+    if (!a_scales || !w_scales) return DPTQ_ERR_INVALID_ARG;
+    if (!aligned16(a_scales) || !aligned16(w_scales) || !aligned16(y)) return DPTQ_ERR_INVALID_ARG;
+    return from_hip(dptq::launch_qlinear(codes, a_scales, M, (int)K, bits, w_packed, w_scales, N,
+                                         y, nullptr, kernel, static_cast<hipStream_t>(stream)));
+  }
+  if (!aligned16(acc)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_qlinear(codes, nullptr, M, (int)K, bits, w_packed, nullptr, N,
+                                       nullptr, acc, kernel, static_cast<hipStream_t>(stream)));
 }
 
 int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {

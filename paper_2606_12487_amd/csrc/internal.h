@@ -23,10 +23,16 @@ hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
 hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
                                   uint8_t* w_packed, float* w_scales,
                                   hipStream_t stream);
+// GEMM kernels (values of dptq_gemm_kernel).
+constexpr int kGemmAuto = 0, kGemmDecode = 1, kGemmTile = 2, kGemmWide = 3;
+
+// Whether a kernel covers the shape (kGemmAuto and kGemmTile cover all).
+bool gemm_kernel_fits(int kernel, int64_t M, int64_t N, int K, int bits);
+
 // out_acc != nullptr selects the raw int32 accumulator output.
 hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
                           int K, int bits, const uint8_t* w_packed,
                           const float* w_scales, int64_t N, void* y,
-                          int32_t* out_acc, hipStream_t stream);
+                          int32_t* out_acc, int kernel, hipStream_t stream);
 
 }  // namespace dptq

@@ -86,8 +86,7 @@ __device__ __forceinline__ __half dequant(int acc, float as, float ws) {
 //
 // The instantiated shape is 256 x 128 on eight wavefronts of 64 x 64, two
 // per SIMD: one wavefront's unpack and LDS reads co-execute with the other's
-// MFMAs.  (A 192 x 256 tile on four wavefronts of 96 x 128 moves fewer LDS
-// bytes per MFMA but, at one wavefront per SIMD, measured slower.)
+// MFMAs.  Large problems use the wide-tile kernel further below instead.
 // ---------------------------------------------------------------------------
 constexpr int kBK = 256;
 
@@ -101,6 +100,14 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 // Address = wavefront-uniform base + 32-bit per-lane offset.
 __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_off) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_off)
+               : "memory", "m0");
+}
+
+// The same with 4 bytes per lane (LDS byte offset lds_off + 4 * lane).
+__device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, uint32_t lds_off) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
                :
                : "v"(voff), "s"(sbase), "s"(lds_off)
                : "memory", "m0");
@@ -450,6 +457,366 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
 }
 
 // ---------------------------------------------------------------------------
+// Prefill, wide wavefront tiles: 192 (n) x 256 (m) output tiles on four
+// wavefronts, one per SIMD, each owning 96 x 128 = 3 x 4 MFMAs of 32 x 32 x
+// 32.  Every unpacked fragment feeds three or four MFMAs, so unpacking costs
+// 3.5 VALU instructions per MFMA with 4-bit activations (6 with 64 x 64
+// wavefront tiles) and the VALU work fits beside the matrix pipe.
+//
+// The kernel is persistent: one workgroup per compute unit walks its tiles,
+// and the load ring runs on across tile boundaries, so the first stages of
+// the next tile are in flight while a tile's epilogue runs.  Output rows
+// leave straight from registers (two lanes' halves of a row are joined with
+// a cross-lane swap), which keeps LDS free for the ring.  The activation and
+// weight scales of a tile arrive in LDS by the same direct loads.
+//
+// With one wavefront per SIMD nothing else hides latency, so the k loop is
+// pipelined explicitly, one 32-k MFMA step at a time: a step's LDS reads are
+// issued two steps before its MFMAs, its unpack one step before, and the
+// MFMAs of a step are interleaved one by one with the next step's unpack.
+// Stages are 128 k (64-byte slices of 4-bit rows) in a ring of four load
+// buffers (three for 8-bit activations); the barrier that opens stage g + 1
+// sits in the middle of stage g, once every LDS read of stage g has
+// returned.  Tiles at the matrix edge are shifted inward to end at the edge
+// (they recompute, and rewrite with identical values, a strip of their
+// neighbour), so every tile is full and the loads need no clamping.
+// ---------------------------------------------------------------------------
+template <int BITS>
+struct Wide {
+  static constexpr int kBN = 192, kBM = 256, kTI = 3, kTJ = 4;
+  static constexpr int kWaves = 4, kThreads = 256, kBK = 128;
+  static constexpr int kWRow = kBK / 2;                      // 64 B
+  static constexpr int kARow = BITS == 4 ? kBK / 2 : kBK;    // 64 or 128 B
+  static constexpr int kW = kBN * kWRow;
+  static constexpr int kA = kBM * kARow;
+  static constexpr int kStage = kW + kA;
+  static constexpr int kBufs = BITS == 4 ? 4 : 3;
+  static constexpr int kRing = kBufs * kStage;
+  // Two slots (tile parity) of scales: a_s [256] at +0, w_s [192] at +1024.
+  static constexpr int kScaleSlot = 2048;
+  static_assert(kBM % 64 == 0 && kBN % 64 == 0 && kBM * 4 <= 1024 && kBN * 4 <= kScaleSlot - 1024,
+                "scale slots");
+  static constexpr int kLds = kRing + 2 * kScaleSlot;
+  static constexpr int kWLoads = kW / 1024 / kWaves;         // per wavefront and stage
+  static constexpr int kALoads = kA / 1024 / kWaves;
+  static constexpr int kLoads = kWLoads + kALoads;
+  static constexpr int kAReads = BITS == 4 ? 1 : 2;          // 16-byte reads per A fragment per chunk
+  static constexpr int kReads = kTI + kTJ * kAReads;         // per chunk
+  // VALU instructions of one step's unpack: 6 per 4-bit fragment, 4 per
+  // 8-bit one, spread over the step's 12 MFMAs as kVHi after each of the
+  // first kNHi and kVHi - 1 after the rest.
+  static constexpr int kValu = 6 * kTI + (BITS == 4 ? 6 : 4) * kTJ;
+  static constexpr int kMfma = kTI * kTJ;
+  static constexpr int kVHi = (kValu + kMfma - 1) / kMfma;
+  static constexpr int kNHi = kValu - (kVHi - 1) * kMfma;
+  // The ring holds stages of at most two consecutive tiles: K >= kBufs stages.
+  static constexpr int kMinK = kBufs * kBK;
+  static_assert(kLds <= 160 * 1024, "LDS budget");
+  static_assert(kW % (1024 * kWaves) == 0 && kA % (1024 * kWaves) == 0, "load split");
+};
+
+// Scheduling groups for one step: MFMA q, then kVHi (q < kNHi) or kVHi - 1
+// VALU instructions, then one LDS read while reads remain.
+template <int Q, int NM, int VHI, int NHI, int NR>
+__device__ __forceinline__ void sched_step() {
+  if constexpr (Q < NM) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, Q < NHI ? VHI : VHI - 1, 0);
+    if constexpr (Q < NR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    sched_step<Q + 1, NM, VHI, NHI, NR>();
+  }
+}
+
+// Four accumulators of one lane, dequantized and packed as fp16.
+template <int BITS>
+__device__ __forceinline__ uint2 dequant4(int a0, int a1, int a2, int a3, float as, float4 ws) {
+  const __half h0 = dequant(unscale<BITS>(a0), as, ws.x);
+  const __half h1 = dequant(unscale<BITS>(a1), as, ws.y);
+  const __half h2 = dequant(unscale<BITS>(a2), as, ws.z);
+  const __half h3 = dequant(unscale<BITS>(a3), as, ws.w);
+  uint2 pk;
+  pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
+  pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
+  return pk;
+}
+
+template <int BITS, bool ACC_OUT>
+__global__ void __launch_bounds__(256)
+qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
+                   const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
+                   int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
+  using C = Wide<BITS>;
+  constexpr int kTI = C::kTI, kTJ = C::kTJ, kB = C::kBufs;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[C::kLds];
+
+  const int tiles_m = (M + C::kBM - 1) / C::kBM;
+  const int tiles_n = (N + C::kBN - 1) / C::kBN;
+  const int total = tiles_m * tiles_n;
+  const int G = gridDim.x;                                       // <= total
+  const int ntile = (total - (int)blockIdx.x + G - 1) / G;       // tiles of this workgroup, >= 1
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wn = wave & 1, wm = wave >> 1;
+  const int wrow = K / 2;
+  const int arow = BITS == 4 ? K / 2 : K;
+  const int nst = K / C::kBK;
+
+  // Row origins of this workgroup's tile r.  Consecutive tiles of one XCD's
+  // workgroups are consecutive logical tiles (m fastest), so they share
+  // weight rows in that XCD's L2.
+  auto origin = [&](int r, int& m0, int& n0) __attribute__((always_inline)) {
+    const int logical = xcd_remap((int)blockIdx.x + r * G, total);
+    const int tm = logical % tiles_m, tn = logical / tiles_m;
+    m0 = min(tm * C::kBM, M - C::kBM);
+    n0 = min(tn * C::kBN, N - C::kBN);
+  };
+
+  // Direct loads.  One load instruction fills 1 KiB of LDS: 16 rows of 64 B
+  // (4-bit operands) or 8 rows of 128 B (8-bit activations).  Lane l writes
+  // physical chunk p of its row r, which holds logical chunk p ^ sw(r), with
+  // sw(r) = (r >> 2) & 3 for 64-byte rows and (r >> 1) & 7 for 128-byte
+  // rows.  Load i of wavefront w fills LDS block j = 4 i + w, rows 16 j +
+  // (l >> 2) (resp. 8 j + (l >> 3)), so sw depends on the lane (and on w & 1)
+  // only and the row part of the address is wavefront-uniform.
+  constexpr int kARows = BITS == 4 ? 16 : 8;
+  const uint32_t wlane = (uint32_t)((lane >> 2) * wrow + (((lane & 3) ^ ((lane >> 4) & 3)) * 16));
+  const uint32_t alane =
+      BITS == 4 ? (uint32_t)((lane >> 2) * arow + (((lane & 3) ^ ((lane >> 4) & 3)) * 16))
+                : (uint32_t)((lane >> 3) * arow + (((lane & 7) ^ ((4 * (wave & 1) + (lane >> 4)) & 7)) * 16));
+  const uint32_t smem_base = (uint32_t)(uintptr_t)(lds_ptr)smem;
+  auto issue = [&](int m0, int n0, int st, int buf) __attribute__((always_inline)) {
+    const uint32_t base = smem_base + buf * C::kStage + wave * 1024;
+    const uint8_t* wt = w_packed + (size_t)n0 * wrow + (size_t)st * C::kWRow;   // uniform
+    const uint8_t* at = a_codes + (size_t)m0 * arow + (size_t)st * C::kARow;    // uniform
+#pragma unroll
+    for (int i = 0; i < C::kWLoads; ++i)
+      dma16(wt + (size_t)((4 * i + wave) * 16) * wrow, wlane, base + i * 4096);
+#pragma unroll
+    for (int i = 0; i < C::kALoads; ++i)
+      dma16(at + (size_t)((4 * i + wave) * kARows) * arow, alane, base + C::kW + i * 4096);
+  };
+  // Scales of a tile into slot q (only when producing y; the accumulator
+  // output has none): wavefront 0 loads a_s [256] in four 4-byte-per-lane
+  // loads (a shifted tile's m0 need not be 16-byte aligned), wavefront 1
+  // w_s [192] in three.  Extra loads only make the other wavefronts' waits
+  // stricter, never weaker.
+  auto issue_scales = [&](int m0, int n0, int q) __attribute__((always_inline)) {
+    if constexpr (!ACC_OUT) {
+      const uint32_t base = smem_base + C::kRing + q * C::kScaleSlot;
+      if (wave == 0) {
+#pragma unroll
+        for (int i = 0; i < C::kBM / 64; ++i) dma4(a_scales + m0 + 64 * i, (uint32_t)lane * 4, base + 256 * i);
+      } else if (wave == 1) {
+#pragma unroll
+        for (int i = 0; i < C::kBN / 64; ++i)
+          dma4(w_scales + n0 + 64 * i, (uint32_t)lane * 4, base + 1024 + 256 * i);
+      }
+    }
+  };
+
+  // Fragment reads.  In chunk e (64 k) of a stage, lane l reads row l & 31 of
+  // each 32-row tile, logical 16-byte chunk 2 g + e of a 64-byte row (g = l >>
+  // 5), or chunks 4 g + 2 e and 4 g + 2 e + 1 of a 128-byte row: 32 k per
+  // lane, two MFMA steps.  Fragment rows are 32 t + (l & 31) plus a multiple of
+  // 32, so sw(row) depends on the lane only and the tile enters as an
+  // immediate offset.
+  const int fr = lane & 31, fg = lane >> 5;
+  const int sw4 = (fr >> 2) & 3, sw8 = (fr >> 1) & 7;
+  uint32_t wv[2], av[4];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    wv[e] = (uint32_t)((wn * kTI * 32 + fr) * C::kWRow + (((2 * fg + e) ^ sw4) * 16));
+    if (BITS == 4) av[e] = (uint32_t)(C::kW + (wm * kTJ * 32 + fr) * C::kARow + (((2 * fg + e) ^ sw4) * 16));
+  }
+  if (BITS == 8) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      av[c] = (uint32_t)(C::kW + (wm * kTJ * 32 + fr) * C::kARow + (((4 * fg + c) ^ sw8) * 16));
+  }
+
+  struct Packed {
+    uint32_t w[kTI][4];
+    uint32_t a[kTJ][4 * C::kAReads];
+  };
+  struct Ops {
+    v4i w[kTI];
+    v4i a[kTJ];
+  };
+  auto read_chunk = [&](int buf, int e, Packed& p) __attribute__((always_inline)) {
+    const uint8_t* s = smem + buf * C::kStage;
+#pragma unroll
+    for (int i = 0; i < kTI; ++i) {
+      const uint4 v = *reinterpret_cast<const uint4*>(s + wv[e] + i * 32 * C::kWRow);
+      p.w[i][0] = v.x; p.w[i][1] = v.y; p.w[i][2] = v.z; p.w[i][3] = v.w;
+    }
+#pragma unroll
+    for (int j = 0; j < kTJ; ++j) {
+#pragma unroll
+      for (int q = 0; q < C::kAReads; ++q) {
+        const uint32_t off = BITS == 4 ? av[e] : av[2 * e + q];
+        const uint4 v = *reinterpret_cast<const uint4*>(s + off + j * 32 * C::kARow);
+        p.a[j][4 * q] = v.x; p.a[j][4 * q + 1] = v.y; p.a[j][4 * q + 2] = v.z; p.a[j][4 * q + 3] = v.w;
+      }
+    }
+  };
+  // MFMA operands of step kk (32 k) of a chunk.
+  auto unpack = [&](const Packed& p, int kk, Ops& o) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kTI; ++i) o.w[i] = op_from_nibbles(p.w[i][2 * kk], p.w[i][2 * kk + 1]);
+#pragma unroll
+    for (int j = 0; j < kTJ; ++j) {
+      if (BITS == 4) o.a[j] = op_from_nibbles(p.a[j][2 * kk], p.a[j][2 * kk + 1]);
+      else o.a[j] = op_from_bytes(p.a[j][4 * kk], p.a[j][4 * kk + 1], p.a[j][4 * kk + 2], p.a[j][4 * kk + 3]);
+    }
+  };
+  v16i acc[kTI][kTJ];
+  auto mfmas = [&](const Ops& o) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kTI; ++i)
+#pragma unroll
+      for (int j = 0; j < kTJ; ++j) acc[i][j] = mfma32(o.w[i], o.a[j], acc[i][j]);
+  };
+  constexpr int kNM = C::kMfma, kVH = C::kVHi, kNH = C::kNHi, kNR = C::kReads;
+
+  // Epilogue of the tile at (m0, n0) with its scales in slot q.  Lane l holds
+  // column m = l & 31 of each 32 x 32 accumulator and, in registers 4b ..
+  // 4b+3, rows n = 8 b + 4 g + 0..3.  For b = 2p, 2p + 1 a swap of the upper
+  // half-wavefront's first value with the lower half's second gives lane l <
+  // 32 the halves n = 16 p + 0..7 and lane l + 32 the halves 16 p + 8..15 of
+  // row m: one 16-byte store each.
+  auto epilogue = [&](int m0, int n0, int q) __attribute__((always_inline)) {
+    const float* sc = reinterpret_cast<const float*>(smem + C::kRing + q * C::kScaleSlot);
+    const int mbase = wm * kTJ * 32 + fr, nbase = wn * kTI * 32;
+    if (ACC_OUT) {
+#pragma unroll
+      for (int j = 0; j < kTJ; ++j) {
+        const int m = m0 + mbase + j * 32;
+#pragma unroll
+        for (int i = 0; i < kTI; ++i)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int n = n0 + nbase + i * 32 + 8 * b + 4 * fg;
+            *reinterpret_cast<int4*>(acc_out + (size_t)m * N + n) =
+                make_int4(unscale<BITS>(acc[i][j][4 * b]), unscale<BITS>(acc[i][j][4 * b + 1]),
+                          unscale<BITS>(acc[i][j][4 * b + 2]), unscale<BITS>(acc[i][j][4 * b + 3]));
+          }
+      }
+      return;
+    }
+#pragma unroll
+    for (int j = 0; j < kTJ; ++j) {
+      const float as = sc[mbase + j * 32];
+      const int m = m0 + mbase + j * 32;
+#pragma unroll
+      for (int i = 0; i < kTI; ++i) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int nl = nbase + i * 32 + 16 * p + 4 * fg;
+          const float4 ws0 = *reinterpret_cast<const float4*>(sc + 256 + nl);
+          const float4 ws1 = *reinterpret_cast<const float4*>(sc + 256 + nl + 8);
+          const uint2 x0 = dequant4<BITS>(acc[i][j][8 * p], acc[i][j][8 * p + 1], acc[i][j][8 * p + 2],
+                                          acc[i][j][8 * p + 3], as, ws0);
+          const uint2 x1 = dequant4<BITS>(acc[i][j][8 * p + 4], acc[i][j][8 * p + 5], acc[i][j][8 * p + 6],
+                                          acc[i][j][8 * p + 7], as, ws1);
+          const auto s0 = __builtin_amdgcn_permlane32_swap(x0.x, x1.x, false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(x0.y, x1.y, false, false);
+          const int n = n0 + nbase + i * 32 + 16 * p + 8 * fg;
+          *reinterpret_cast<uint4*>(y + (size_t)m * N + n) = make_uint4(s0[0], s1[0], s0[1], s1[1]);
+        }
+        // One accumulator at a time: keeps the scheduler from reading all of
+        // them out of the accumulator registers at once.
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
+  // Ring: global stage g (stage g mod nst of tile g / nst) lives in buffer
+  // g mod kB.  The loads of stage g + kB - 1 are issued at the barrier that
+  // opens stage g, into the buffer of stage g - 1 (every wavefront has waited
+  // for all its reads of it by then).  Every barrier issues exactly one stage
+  // (after the last tile's end the last stage again, into a buffer nobody
+  // reads any more), so at the barrier opening stage g the kB - 2 stages
+  // after it are exactly the loads allowed in flight.
+  Packed p0, p1;
+  Ops u0, u1;
+  int m0, n0;
+  origin(0, m0, n0);
+  issue_scales(m0, n0, 0);
+#pragma unroll
+  for (int st = 0; st < kB - 1; ++st) issue(m0, n0, st, st);
+  wait_vmcnt<(kB - 2) * C::kLoads>();
+  lds_barrier();
+  issue(m0, n0, kB - 1, kB - 1);
+  read_chunk(0, 0, p0);
+  unpack(p0, 0, u0);
+  int cur = 0;   // buffer of the current stage
+  for (int r = 0; r < ntile; ++r) {
+    const bool has_next = r + 1 < ntile;
+    int m1 = m0, n1 = n0;
+    if (has_next) origin(r + 1, m1, n1);
+#pragma unroll
+    for (int i = 0; i < kTI; ++i)
+#pragma unroll
+      for (int j = 0; j < kTJ; ++j) acc[i][j] = v16i{};
+    for (int s = 0; s < nst - 1; ++s) {
+      const int nxt = cur + 1 == kB ? 0 : cur + 1;
+      read_chunk(cur, 1, p1);
+      mfmas(u0);
+      unpack(p0, 1, u1);
+      sched_step<0, kNM, kVH, kNH, kNR>();
+      mfmas(u1);
+      unpack(p1, 0, u0);
+      sched_step<0, kNM, kVH, kNH, 0>();
+      wait_vmcnt<(kB - 2) * C::kLoads>();
+      lds_barrier();
+      // Stage s + kB of this tile, or of the next one (after the last tile:
+      // this tile's last stage again).
+      const int si = s + kB;
+      const bool in_next = si >= nst;
+      issue(in_next ? m1 : m0, in_next ? n1 : n0, in_next ? (has_next ? si - nst : nst - 1) : si, cur);
+      read_chunk(nxt, 0, p0);
+      mfmas(u0);
+      unpack(p1, 1, u1);
+      sched_step<0, kNM, kVH, kNH, kNR>();
+      mfmas(u1);
+      unpack(p0, 0, u0);
+      sched_step<0, kNM, kVH, kNH, 0>();
+      cur = nxt;
+    }
+    {
+      // Last stage: the next tile's first chunk is read only after the
+      // epilogue, so that no operand registers are held across it.
+      read_chunk(cur, 1, p1);
+      mfmas(u0);
+      unpack(p0, 1, u1);
+      sched_step<0, kNM, kVH, kNH, kNR>();
+      mfmas(u1);
+      unpack(p1, 0, u0);
+      sched_step<0, kNM, kVH, kNH, 0>();
+      if (has_next) {
+        wait_vmcnt<(kB - 2) * C::kLoads>();
+        lds_barrier();
+        issue(m1, n1, kB - 1, cur);
+        issue_scales(m1, n1, (r + 1) & 1);
+      }
+      mfmas(u0);
+      unpack(p1, 1, u1);
+      sched_step<0, kNM, kVH, kNH, 0>();
+      mfmas(u1);
+      cur = cur + 1 == kB ? 0 : cur + 1;
+    }
+    epilogue(m0, n0, r & 1);
+    if (has_next) {
+      read_chunk(cur, 0, p0);
+      unpack(p0, 0, u0);
+    }
+    m0 = m1;
+    n0 = n1;
+  }
+  wait_vmcnt<0>();   // the re-issued tail loads land before the workgroup's LDS is released
+}
+
+// ---------------------------------------------------------------------------
 // Decode (M <= 16): one workgroup per 16 output channels; its 8 wavefronts
 // split K, stream the weight rows once with 16-byte loads, and the int32
 // partial tiles are summed exactly in LDS.
@@ -543,34 +910,111 @@ void launch_prefill(const uint8_t* a, const float* as, int64_t M, int K, const u
 }
 
 template <int BITS, bool ACC_OUT>
+void launch_wide(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
+                 const float* ws, int64_t N, __half* y, int32_t* acc, int cus, hipStream_t stream) {
+  using C = Wide<BITS>;
+  const int64_t tiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
+  const int64_t grid = tiles < cus ? tiles : cus;
+  hipLaunchKernelGGL((qgemm_prefill_wide<BITS, ACC_OUT>), dim3((unsigned)grid), dim3(C::kThreads), 0,
+                     stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+      v = 256;
+    cache[dev] = v;
+  }
+  return cache[dev];
+}
+
+// Relative time of a launch: rounds of one tile per compute unit, times the
+// tile's area over the measured throughput of the tile shape.
+double launch_cost(int64_t M, int64_t N, int bm, int bn, double speed, int cus) {
+  const int64_t tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  return (double)((tiles + cus - 1) / cus) * (double)bm * (double)bn / speed;
+}
+
+// Throughput of the wide tiles per unit of tile area relative to the
+// 256 x 128 tiles (measured on large prefill shapes).
+constexpr double kWideSpeed = 1.3;
+
+template <int BITS>
+bool wide_fits(int64_t M, int64_t N, int K) {
+  using W = Wide<BITS>;
+  return M >= W::kBM && N >= W::kBN && K >= W::kMinK;
+}
+
+// Kernel for a shape: M <= 16 streams the weights; otherwise the tile shape
+// with the smaller estimated time (the wide tiles need at least one full
+// tile and a ring's worth of k).
+template <int BITS>
+int auto_kernel(int64_t M, int64_t N, int K) {
+  if (M <= 16) return kGemmDecode;
+  using S = PrefillCfg<BITS>;
+  using W = Wide<BITS>;
+  const int cus = device_cus();
+  if (wide_fits<BITS>(M, N, K) &&
+      launch_cost(M, N, W::kBM, W::kBN, kWideSpeed, cus) <= launch_cost(M, N, S::kBM, S::kBN, 1.0, cus))
+    return kGemmWide;
+  return kGemmTile;
+}
+
+template <int BITS, bool ACC_OUT>
 hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
                     const uint8_t* w, const float* ws, int64_t N, __half* y,
-                    int32_t* acc, hipStream_t stream) {
+                    int32_t* acc, int kernel, hipStream_t stream) {
   if (M == 0) return hipSuccess;
-  if (M <= 16) {
-    hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT>), dim3((unsigned)(N / 16)),
-                       dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
-  } else {
-    launch_prefill<PrefillCfg<BITS>, ACC_OUT>(a, as, M, K, w, ws, N, y, acc, stream);
+  if (kernel == kGemmAuto) kernel = auto_kernel<BITS>(M, N, K);
+  switch (kernel) {
+    case kGemmDecode:
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT>), dim3((unsigned)(N / 16)),
+                         dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+      break;
+    case kGemmWide:
+      launch_wide<BITS, ACC_OUT>(a, as, M, K, w, ws, N, y, acc, device_cus(), stream);
+      break;
+    default:
+      launch_prefill<PrefillCfg<BITS>, ACC_OUT>(a, as, M, K, w, ws, N, y, acc, stream);
+      break;
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
+bool gemm_kernel_fits(int kernel, int64_t M, int64_t N, int K, int bits) {
+  switch (kernel) {
+    case kGemmAuto:
+    case kGemmTile:
+      return true;
+    case kGemmDecode:
+      return M <= 16;
+    case kGemmWide:
+      return bits == 4 ? wide_fits<4>(M, N, K) : wide_fits<8>(M, N, K);
+    default:
+      return false;
+  }
+}
+
 hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M, int K,
                           int bits, const uint8_t* w_packed, const float* w_scales,
-                          int64_t N, void* y, int32_t* out_acc, hipStream_t stream) {
+                          int64_t N, void* y, int32_t* out_acc, int kernel, hipStream_t stream) {
   const uint8_t* a = static_cast<const uint8_t*>(codes);
   __half* yh = static_cast<__half*>(y);
   if (out_acc) {
     if (bits == 4)
-      return launch_t<4, true>(a, a_scales, M, K, w_packed, w_scales, N, yh, out_acc, stream);
-    return launch_t<8, true>(a, a_scales, M, K, w_packed, w_scales, N, yh, out_acc, stream);
+      return launch_t<4, true>(a, a_scales, M, K, w_packed, w_scales, N, yh, out_acc, kernel, stream);
+    return launch_t<8, true>(a, a_scales, M, K, w_packed, w_scales, N, yh, out_acc, kernel, stream);
   }
   if (bits == 4)
-    return launch_t<4, false>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr, stream);
-  return launch_t<8, false>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr, stream);
+    return launch_t<4, false>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr, kernel, stream);
+  return launch_t<8, false>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr, kernel, stream);
 }
 
 }  // namespace dptq

@@ -124,6 +124,30 @@ def test_qlinear_acc_validation(L):
     assert f(FAKE, 0, 256, 8, NULL, 64, NULL, NULL) == OK
 
 
+def qk(L, codes=FAKE, a_s=FAKE, M=300, K=1024, bits=4, w=FAKE, w_s=FAKE, N=272, y=FAKE,
+       acc=NULL, kernel=0):
+    return L.dptq_qlinear_kernel(codes, a_s, M, K, bits, w, w_s, N, y, acc, kernel, NULL)
+
+
+def test_qlinear_kernel_validation(L):
+    assert qk(L, kernel=-1) == INVALID
+    assert qk(L, kernel=4) == INVALID
+    assert qk(L, acc=FAKE) == INVALID                       # both y and acc
+    assert qk(L, y=NULL) == INVALID                         # neither
+    assert qk(L, kernel=dptq.GEMM_DECODE) == UNSUPPORTED    # M > 16
+    assert qk(L, kernel=dptq.GEMM_TILE_192X256, M=255) == UNSUPPORTED
+    assert qk(L, kernel=dptq.GEMM_TILE_192X256, N=176) == UNSUPPORTED
+    assert qk(L, kernel=dptq.GEMM_TILE_192X256, K=384) == UNSUPPORTED
+    assert qk(L, K=200) == UNSUPPORTED
+    for name in ("codes", "a_s", "w", "w_s"):
+        assert qk(L, **{name: NULL}) == INVALID, name
+        assert qk(L, **{name: MISALIGNED}) == INVALID, name
+    # the accumulator output ignores the scales
+    assert qk(L, M=0, y=NULL, acc=FAKE, a_s=NULL, w_s=NULL, codes=NULL, w=NULL) == OK
+    assert qk(L, y=NULL, acc=MISALIGNED, a_s=NULL, w_s=NULL) == INVALID
+    assert qk(L, M=0, kernel=dptq.GEMM_DECODE, codes=NULL, a_s=NULL, w=NULL, w_s=NULL) == OK
+
+
 def test_prepare_weights_validation(L):
     f = L.dptq_prepare_weights
     assert f(FAKE, 16, 256, 100, FAKE, FAKE, NULL) == INVALID

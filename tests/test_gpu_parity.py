@@ -207,8 +207,26 @@ GEMM_CASES = [
     (16, 256, 512, None), (17, 128, 16, None), (300, 1024, 272, None),
     (1, 14336, 4096, None), (4, 14336, 4096, None), (8, 8192, 1024, None),
     (16, 14336, 4096, None), (5, 11008, 64, None), (129, 4096, 528, None),
+    (256, 512, 192, None), (511, 640, 400, None),
     (2048, 4096, 12288, 48), (2048, 14336, 4096, 32), (4096, 8192, 1024, 32),
+    (2100, 1024, 12304, 48),
 ]
+
+# Every kernel must return the same bits; each case runs the automatic
+# choice and every kernel whose range covers the shape.
+KERNELS = (dptq.GEMM_DECODE, dptq.GEMM_TILE_256X128, dptq.GEMM_TILE_192X256)
+
+
+def _fits(kernel, M, K, N):
+    if kernel == dptq.GEMM_DECODE:
+        return M <= 16
+    if kernel == dptq.GEMM_TILE_192X256:
+        return M >= 256 and N >= 192 and K >= 512
+    return True
+
+
+def _kernels_for(M, K, N):
+    return [dptq.GEMM_AUTO] + [k for k in KERNELS if _fits(k, M, K, N)]
 
 
 def _gemm_inputs(M, K, N, bits, seed):
@@ -224,30 +242,33 @@ def _gemm_inputs(M, K, N, bits, seed):
 @pytest.mark.parametrize("M,K,N,ns", GEMM_CASES)
 def test_gemm_acc_and_output(dev, M, K, N, ns, bits):
     a, w, a_s, w_s = _gemm_inputs(M, K, N, bits, M + K + N + bits)
-    ad, wd = _d(a, dev), _d(w, dev)
-    acc = _h(dptq.qlinear_acc(ad, bits, wd))
-    y = _h(dptq.qlinear(ad, _d(a_s, dev), bits, wd, _d(w_s, dev)))
+    ad, wd, asd, wsd = _d(a, dev), _d(w, dev), _d(a_s, dev), _d(w_s, dev)
     rows = np.arange(M) if ns is None else _sample_rows(M, ns, np.random.default_rng(M))
     acc_ref = qlinear_acc_ref(a[rows], bits, w)
-    assert np.array_equal(acc[rows].astype(np.int64), acc_ref), \
-        f"{(acc[rows] != acc_ref).sum()} accumulators differ"
-    _assert_f16(y[rows], epilogue_ref(acc_ref, a_s[rows], w_s), f"y M={M} K={K} N={N}")
+    y_ref = epilogue_ref(acc_ref, a_s[rows], w_s)
+    for kernel in _kernels_for(M, K, N):
+        acc = _h(dptq.qlinear_acc(ad, bits, wd, kernel=kernel))
+        y = _h(dptq.qlinear(ad, asd, bits, wd, wsd, kernel=kernel))
+        assert np.array_equal(acc[rows].astype(np.int64), acc_ref), \
+            f"kernel {kernel}: {(acc[rows] != acc_ref).sum()} accumulators differ"
+        _assert_f16(y[rows], y_ref, f"kernel {kernel}: y M={M} K={K} N={N}")
 
 
 @pytest.mark.parametrize("bits", [4, 8])
-@pytest.mark.parametrize("M", [3, 40])
-def test_gemm_extreme_accumulators(dev, bits, M):
+@pytest.mark.parametrize("M,N", [(3, 32), (40, 32), (256, 192)])
+def test_gemm_extreme_accumulators(dev, bits, M, N):
     # Largest magnitudes at the largest K: all activation codes at their
     # minimum and all weights at -8 give acc = K * 8 * |a_min| per entry.
-    K, N = 65536, 32
+    K = 65536
     a = (np.full((M, K // 2), 0x88, np.uint8) if bits == 4
          else np.full((M, K), -128, np.int8))
     w = np.full((N, K // 2), 0x88, np.uint8)
     w[1::2] = 0x77                      # +7 rows: negative accumulators
-    acc = _h(dptq.qlinear_acc(_d(a, dev), bits, _d(w, dev)))
     ref = qlinear_acc_ref(a, bits, w)
-    assert np.array_equal(acc.astype(np.int64), ref)
     assert int(np.abs(ref).max()) == K * 8 * (8 if bits == 4 else 128)
+    for kernel in _kernels_for(M, K, N):
+        acc = _h(dptq.qlinear_acc(_d(a, dev), bits, _d(w, dev), kernel=kernel))
+        assert np.array_equal(acc.astype(np.int64), ref), f"kernel {kernel}"
 
 
 def test_gemm_entries_cross_check(dev):
