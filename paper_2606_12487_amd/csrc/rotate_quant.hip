@@ -9,6 +9,12 @@
 // reduced across the workgroup, and the final pass divides, rounds to nearest
 // even, packs and stores the codes with coalesced writes.
 //
+// Two kernels: a register-phase kernel for power-of-two sizes up to 4096 (the
+// sizes of every LLaMA projection except the largest ones), and a general
+// kernel for the others (28 * 2^j, and 2^j above 4096).  Both are limited by
+// vector ALU issue, not by memory: the fp32 butterflies alone are log2(h)
+// instructions per element, and packed fp32 arithmetic is not used.
+//
 // Quotient: t = fl32(y / s) is formed as q = y * r, e = fma(-q, s, y),
 // t = fma(e, r, q) with r = fl32(1 / s) (Markstein's correction, one
 // correctly rounded reciprocal per row), which returns the correctly rounded
@@ -284,11 +290,253 @@ hipError_t dispatch_j(int j, const Tin* x, int64_t M, int K, uint8_t* codes, flo
   }
 }
 
+// ---------------------------------------------------------------------------
+// Power-of-two Hadamard sizes up to 4096.  The row sits in LDS as 4096-element
+// segments (the last one zero-padded); in every phase each of the 256 threads
+// holds 16 elements of a segment in registers, so the 12 index bits of a
+// segment are covered by three register phases of 4 bits each:
+//   phase 1: thread t holds i = 16 t + r        (register bits = index bits 0-3)
+//   phase 2: thread t holds i = 256 (t >> 4) + 16 r + (t & 15)   (bits 4-7)
+//   phase 3: thread t holds i = 256 r + t                        (bits 8-11)
+// and the stages run in the order bit 0, 1, 2, ...  Element i of a segment
+// sits at float offset i + 4 (i >> 6): every phase's accesses are then free
+// of bank conflicts and their addresses are a per-thread base plus
+// compile-time offsets.  Phase 1 loads from global memory and the final pass
+// re-reads the phase-1 layout to quantize 16 consecutive elements per thread.
+//
+// Codes are rounded with the fp32 adder: t + 1.5 * 2^23 rounds t to the
+// nearest integer, ties to even, and leaves it in the low mantissa bits
+// (two's complement), from which nibbles and bytes are packed with byte
+// permutes and one bit-field insert.  |code| <= qmax holds without a clamp:
+// |t| <= fl32(amax / s) with s = fl32(amax / qmax) rounds to at most qmax.
+// ---------------------------------------------------------------------------
+constexpr int kSeg = 4096;
+constexpr int kSegFloats = kSeg + kSeg / 16;        // 4 floats of padding per 64
+__device__ __forceinline__ int seg_off(int i) { return i + 4 * (i >> 6); }
+
+// Butterflies over bit B of the register index of v[16] (stride 2^B).
+template <int B>
+__device__ __forceinline__ void stage16(float* v) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    if (r & (1 << B)) continue;
+    const float a = v[r], c = v[r | (1 << B)];
+    v[r] = a + c;
+    v[r | (1 << B)] = a - c;
+  }
+}
+// Register bits [LO, HI) in order.
+template <int LO, int HI>
+__device__ __forceinline__ void stages16(float* v) {
+  if constexpr (LO < HI) {
+    stage16<LO>(v);
+    stages16<LO + 1, HI>(v);
+  }
+}
+
+__device__ __forceinline__ uint32_t round_bits(float y, float s, float r) {
+  const float q = y * r;
+  const float e = __builtin_fmaf(-q, s, y);
+  const float t = __builtin_fmaf(e, r, q);
+  return __float_as_uint(t + 12582912.0f);          // 1.5 * 2^23
+}
+// Low bytes of four words: [b0, b1, b2, b3].
+__device__ __forceinline__ uint32_t low_bytes(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+  const uint32_t x01 = __builtin_amdgcn_perm(b1, b0, 0x0c0c0400u);
+  const uint32_t x23 = __builtin_amdgcn_perm(b3, b2, 0x0c0c0400u);
+  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
+}
+
+__device__ __forceinline__ float absmax16(const float* v, float m) {
+#pragma unroll
+  for (int r = 0; r < 16; r += 2) m = fmaxf(fmaxf(fabsf(v[r]), fabsf(v[r + 1])), m);
+  return m;
+}
+
+// Maximum over the wavefront of a non-negative float (compared as integer
+// bits, which order non-negative floats): four DPP steps give every lane its
+// 16-lane row maximum, then the four rows are combined as scalars.
+__device__ __forceinline__ float wave_max_nonneg(float m) {
+  int v = __float_as_int(m);
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false));    // quad_perm [1,0,3,2]
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false));    // quad_perm [2,3,0,1]
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false));   // row_half_mirror
+  v = max(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false));   // row_mirror
+  const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+  const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+  return __int_as_float(max(max(r0, r1), max(r2, r3)));
+}
+
+template <typename Tin, int BITS, bool WEIGHT, int J>
+__global__ void __launch_bounds__(kThreads)
+rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
+               float* __restrict__ scales) {
+  static_assert(J <= 12, "segments hold 4096 elements");
+  extern __shared__ float lds[];
+  __shared__ float red[kThreads / 64];
+  const int row = blockIdx.x;
+  const int t = threadIdx.x;
+  const int nseg = (K + kSeg - 1) / kSeg;
+  const Tin* xr = x + (size_t)row * K;
+  constexpr int kLast = J <= 4 ? 1 : (J <= 8 ? 2 : 3);   // last phase with stages
+  // Per-thread LDS bases of the three layouts (segment offset added per use).
+  const int b1 = seg_off(16 * t);
+  const int b2 = seg_off(256 * (t >> 4) + (t & 15));
+  const int b3 = seg_off(t);
+  float tmax = 0.0f;
+
+  for (int sg = 0; sg < nseg; ++sg) {
+    float v[16];
+    const int e = sg * kSeg + 16 * t;
+    // K is a multiple of 8: a thread's second 8 elements may lie past the
+    // row end (then h <= 8 and they form blocks of their own).
+    if (e < K) {
+      load8(xr + e, v);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 8; ++r) v[r] = 0.0f;
+    }
+    if (e + 8 < K) {
+      load8(xr + e + 8, v + 8);
+    } else {
+#pragma unroll
+      for (int r = 8; r < 16; ++r) v[r] = 0.0f;
+    }
+    stages16<0, (J < 4 ? J : 4)>(v);
+    if (kLast == 1) tmax = absmax16(v, tmax);
+    float* sl = lds + sg * kSegFloats + b1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<float4*>(sl + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  }
+  if constexpr (J > 4) {
+    __syncthreads();
+    for (int sg = 0; sg < nseg; ++sg) {
+      float* sl = lds + sg * kSegFloats + b2;
+      float v[16];
+      // i = 256 (t >> 4) + 16 r + (t & 15): offset 16 r + 4 (r >> 2) from b2.
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] = sl[16 * r + 4 * (r >> 2)];
+      stages16<0, (J < 8 ? J : 8) - 4>(v);
+      if (kLast == 2) tmax = absmax16(v, tmax);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sl[16 * r + 4 * (r >> 2)] = v[r];
+    }
+  }
+  if constexpr (J > 8) {
+    __syncthreads();
+    for (int sg = 0; sg < nseg; ++sg) {
+      float* sl = lds + sg * kSegFloats + b3;
+      float v[16];
+      // i = 256 r + t: offset 272 r from b3.
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] = sl[272 * r];
+      stages16<0, J - 8>(v);
+      tmax = absmax16(v, tmax);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sl[272 * r] = v[r];
+    }
+  }
+
+  // Row absmax (padding elements are zero): wavefronts, then the workgroup.
+  tmax = wave_max_nonneg(tmax);
+  if ((t & 63) == 0) red[t >> 6] = tmax;
+  __syncthreads();
+  float amax = red[0];
+#pragma unroll
+  for (int w = 1; w < kThreads / 64; ++w) amax = fmaxf(amax, red[w]);
+
+  constexpr float qmax = (float)((1 << (BITS - 1)) - 1);
+  const float sc = amax / qmax;                 // IEEE division
+  const float rc = sc != 0.0f ? 1.0f / sc : 0.0f;
+  if (t == 0) scales[row] = WEIGHT ? sc / (float)(1 << J) : sc;
+
+  for (int sg = 0; sg < nseg; ++sg) {
+    const int e = sg * kSeg + 16 * t;
+    if (e >= K) continue;
+    const float* sl = lds + sg * kSegFloats + b1;
+    uint32_t bt[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 w4 = *reinterpret_cast<const float4*>(sl + 4 * q);
+      bt[4 * q] = round_bits(w4.x, sc, rc);
+      bt[4 * q + 1] = round_bits(w4.y, sc, rc);
+      bt[4 * q + 2] = round_bits(w4.z, sc, rc);
+      bt[4 * q + 3] = round_bits(w4.w, sc, rc);
+    }
+    const bool full = e + 8 < K;   // else only the first 8 elements are in the row
+    if (BITS == 4) {
+      uint32_t w[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint32_t* b = bt + 8 * h;
+        const uint32_t ev = low_bytes(b[0], b[2], b[4], b[6]);
+        const uint32_t od = low_bytes(b[1], b[3], b[5], b[7]);
+        w[h] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+      }
+      // Rows start 8-byte aligned when K % 32 == 0; otherwise word stores.
+      uint32_t* dst = reinterpret_cast<uint32_t*>(codes + (size_t)row * (K / 2) + e / 2);
+      if (full && K % 32 == 0) {
+        *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+      } else {
+        dst[0] = w[0];
+        if (full) dst[1] = w[1];
+      }
+    } else {
+      uint32_t d[4];
+      d[0] = low_bytes(bt[0], bt[1], bt[2], bt[3]);
+      d[1] = low_bytes(bt[4], bt[5], bt[6], bt[7]);
+      d[2] = low_bytes(bt[8], bt[9], bt[10], bt[11]);
+      d[3] = low_bytes(bt[12], bt[13], bt[14], bt[15]);
+      // Rows start 16-byte aligned when K % 16 == 0, else 8-byte aligned.
+      uint8_t* dst = codes + (size_t)row * K + e;
+      if (full && K % 16 == 0) {
+        *reinterpret_cast<uint4*>(dst) = make_uint4(d[0], d[1], d[2], d[3]);
+      } else {
+        reinterpret_cast<uint2*>(dst)[0] = make_uint2(d[0], d[1]);
+        if (full) reinterpret_cast<uint2*>(dst)[1] = make_uint2(d[2], d[3]);
+      }
+    }
+  }
+}
+
+size_t pow2_lds_bytes(int K) { return (size_t)((K + kSeg - 1) / kSeg) * kSegFloats * sizeof(float); }
+
+template <typename Tin, int BITS, bool WEIGHT, int J>
+hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
+                       hipStream_t stream) {
+  auto kern = rq_pow2_kernel<Tin, BITS, WEIGHT, J>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)pow2_lds_bytes(kMaxRotateK));
+    (void)hipGetLastError();
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(kThreads), pow2_lds_bytes(K), stream, x, K,
+                     codes, scales);
+  return hipGetLastError();
+}
+
+template <typename Tin, int BITS, bool WEIGHT, int J = 0>
+hipError_t dispatch_pow2(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
+                         hipStream_t stream) {
+  if constexpr (J > 12) {
+    return hipErrorInvalidValue;
+  } else {
+    if (j == J) return launch_pow2<Tin, BITS, WEIGHT, J>(x, M, K, codes, scales, stream);
+    return dispatch_pow2<Tin, BITS, WEIGHT, J + 1>(j, x, M, K, codes, scales, stream);
+  }
+}
+
 template <typename Tin, int BITS, bool WEIGHT>
 hipError_t launch_rq(const Tin* x, int64_t M, int K, HadSplit hs, uint8_t* codes,
                      float* scales, hipStream_t stream) {
   if (M == 0) return hipSuccess;
   if (hs.f == 28) return dispatch_j<Tin, BITS, WEIGHT, 28>(hs.j, x, M, K, codes, scales, stream);
+  // Up to 4096 the register-phase kernel; larger sizes the general one.
+  if (hs.j <= 12) return dispatch_pow2<Tin, BITS, WEIGHT>(hs.j, x, M, K, codes, scales, stream);
   return dispatch_j<Tin, BITS, WEIGHT, 1>(hs.j, x, M, K, codes, scales, stream);
 }
 

@@ -74,6 +74,8 @@ ROT_CASES = [
     (3, 112, 28 * 4), (130, 2048, 2048),
     (2, 28672, 28 * 1024), (2, 36864, 4096), (3, 8192, 8192),
     (2, 11008, 256), (16, 256, 256), (2, 28672, 28 * 512),
+    (3, 4096, 512), (2, 16384, 16384), (5, 12288, 4096), (4, 4160, 64),
+    (3, 4224, 128), (2, 4104, 8), (3, 4120, 8),
 ]
 
 
@@ -135,6 +137,21 @@ def test_rotate_quant_special_rows(dev, bits):
     c_ref, s_ref = rotate_quant_ref(x, h, bits)
     _assert_f32(_h(scales), s_ref, "special scales")
     _assert_codes(_h(codes), c_ref, "special codes")
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("K,h", [(4096, 4096), (4096, 256), (14336, 28 * 512), (8192, 8192)])
+def test_rotate_quant_subnormal_inputs(dev, bits, K, h):
+    # Rows of fp16 subnormals and near-subnormal values (exact in fp32): the
+    # rotation must not flush them.
+    rng = np.random.default_rng(K + h + bits)
+    mag = np.exp(rng.uniform(np.log(6e-8), np.log(2e-4), size=(4, K)))
+    x = (mag * rng.choice([-1.0, 1.0], size=(4, K))).astype(np.float16)
+    x[1] = (rng.integers(-1023, 1024, size=K) * 2.0 ** -24).astype(np.float16)   # all subnormal
+    codes, scales = dptq.rotate_quant(_d(x, dev), h, bits)
+    c_ref, s_ref = rotate_quant_ref(x, h, bits)
+    _assert_f32(_h(scales), s_ref, "subnormal scales")
+    _assert_codes(_h(codes), c_ref, "subnormal codes")
 
 
 @pytest.mark.parametrize("bits", [4, 8])
