@@ -101,11 +101,11 @@ __device__ __forceinline__ float absmax8(const float* v, float m) {
 
 // One pass over index bits [s, s+G): each work item gathers the 2^G elements
 // that differ only in those bits, applies the butterflies, and writes back.
-template <int G>
+template <int G, int T>
 __device__ __forceinline__ float pass_bits(float* lds, int K, int s, bool last, float tmax) {
   const int groups = K >> G;
   const int low_mask = (1 << s) - 1;
-  for (int g = threadIdx.x; g < groups; g += kThreads) {
+  for (int g = threadIdx.x; g < groups; g += T) {
     const int base = (g & low_mask) | ((g >> s) << (s + G));
     float v[1 << G];
 #pragma unroll
@@ -121,38 +121,75 @@ __device__ __forceinline__ float pass_bits(float* lds, int K, int s, bool last, 
 }
 
 // Dense 28-point stage: y[b*p + c] = sum over a = 0..27 (in order) of
-// H28[a][b] * z[a*p + c], per block and fast index c.
-__device__ __forceinline__ float pass_28(float* lds, int K, int j, float tmax) {
-  const int p = 1 << j;
-  const int cols = K / 28;
-  for (int col = threadIdx.x; col < cols; col += kThreads) {
-    const int blk = col >> j, c = col & (p - 1);
-    const int base = blk * 28 * p + c;
-    float z[28];
+// H28[a][b] * z[a*p + c], per block and fast index c.  Outputs B0 .. B0+NB-1
+// of one column from its 28 inputs z.
+template <int NB, int B0>
+__device__ __forceinline__ float dense28(float* lds, int base, int p, const float* z, float tmax) {
 #pragma unroll
-    for (int a = 0; a < 28; ++a) z[a] = lds[lidx(base + a * p)];
+  for (int b = B0; b < B0 + NB; ++b) {
+    float acc = kH28.e[0][b] > 0 ? z[0] : -z[0];
 #pragma unroll
-    for (int b = 0; b < 28; ++b) {
-      float acc = kH28.e[0][b] > 0 ? z[0] : -z[0];
-#pragma unroll
-      for (int a = 1; a < 28; ++a) acc = kH28.e[a][b] > 0 ? acc + z[a] : acc - z[a];
-      lds[lidx(base + b * p)] = acc;
-      tmax = fmaxf(tmax, fabsf(acc));
-    }
+    for (int a = 1; a < 28; ++a) acc = kH28.e[a][b] > 0 ? acc + z[a] : acc - z[a];
+    lds[lidx(base + b * p)] = acc;
+    tmax = fmaxf(tmax, fabsf(acc));
   }
   return tmax;
 }
 
-template <int BITS>
-__device__ __forceinline__ int quantize_one(float y, float s, float r) {
-  constexpr int lo = -(1 << (BITS - 1)), hi = (1 << (BITS - 1)) - 1;
+template <int T>
+__device__ __forceinline__ float pass_28(float* lds, int K, int j, float tmax) {
+  const int p = 1 << j;
+  const int cols = K / 28;
+  if (2 * cols <= T && cols % 64 == 0) {
+    // Two threads per column (wavefront-uniform halves), each writing 14 of
+    // its outputs; every input is read before any output is written.
+    const int t = threadIdx.x;
+    const bool active = t < 2 * cols;
+    const int col = t % cols, half = t / cols;
+    const int base = (col >> j) * 28 * p + (col & (p - 1));
+    float z[28];
+    if (active) {
+#pragma unroll
+      for (int a = 0; a < 28; ++a) z[a] = lds[lidx(base + a * p)];
+    }
+    __syncthreads();
+    if (active) {
+      if (half == 0) tmax = dense28<14, 0>(lds, base, p, z, tmax);
+      else tmax = dense28<14, 14>(lds, base, p, z, tmax);
+    }
+    return tmax;
+  }
+  for (int col = threadIdx.x; col < cols; col += T) {
+    const int base = (col >> j) * 28 * p + (col & (p - 1));
+    float z[28];
+#pragma unroll
+    for (int a = 0; a < 28; ++a) z[a] = lds[lidx(base + a * p)];
+    tmax = dense28<28, 0>(lds, base, p, z, tmax);
+  }
+  return tmax;
+}
+
+// Code bits of y / s rounded to nearest, ties to even: t + 1.5 * 2^23 leaves
+// round(t) in the low mantissa bits (two's complement), from which nibbles
+// and bytes are packed.  |code| <= qmax holds without a clamp: |t| <=
+// fl32(amax / s) with s = fl32(amax / qmax) rounds to at most qmax.
+__device__ __forceinline__ uint32_t round_bits(float y, float s, float r) {
   const float q = y * r;
   const float e = __builtin_fmaf(-q, s, y);
   const float t = __builtin_fmaf(e, r, q);
-  int c = (int)__builtin_rintf(t);
-  c = c < lo ? lo : c;
-  c = c > hi ? hi : c;
-  return c;
+  return __float_as_uint(t + 12582912.0f);          // 1.5 * 2^23
+}
+// Low bytes of four words: [b0, b1, b2, b3].
+__device__ __forceinline__ uint32_t low_bytes(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+  const uint32_t x01 = __builtin_amdgcn_perm(b1, b0, 0x0c0c0400u);
+  const uint32_t x23 = __builtin_amdgcn_perm(b3, b2, 0x0c0c0400u);
+  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
+}
+// Eight codes as packed nibbles (element 2j in the low nibble of byte j).
+__device__ __forceinline__ uint32_t pack_nibbles(const uint32_t* b) {
+  const uint32_t ev = low_bytes(b[0], b[2], b[4], b[6]);
+  const uint32_t od = low_bytes(b[1], b[3], b[5], b[7]);
+  return (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
 }
 
 // Compile-time pass plan for h = F * 2^J: the load pass covers index bits
@@ -171,12 +208,12 @@ struct Plan {
   static constexpr int width_from(int s, int left) { return (J - s + left - 1) / left; }
 };
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J>
-__global__ void __launch_bounds__(kThreads)
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T>
+__global__ void __launch_bounds__(T)
 rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
                     float* __restrict__ scales) {
   extern __shared__ float lds[];
-  __shared__ float red[kThreads / 64];
+  __shared__ float red[T / 64];
   using P = Plan<J>;
   static_assert(P::np <= 3, "pass plan too long");
   const int row = blockIdx.x;
@@ -185,7 +222,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
   constexpr bool load_last = (P::np == 0 && F == 1);
 
   float tmax = 0.0f;
-  for (int q = threadIdx.x; q < nchunk; q += kThreads) {
+  for (int q = threadIdx.x; q < nchunk; q += T) {
     float v[8];
     load8(xr + (size_t)q * 8, v);
     butterflies<3>(v, 0, P::j0);
@@ -197,19 +234,19 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
   __syncthreads();
 
   if constexpr (P::np > 0) {
-    tmax = pass_bits<P::width(0)>(lds, K, P::start(0), P::np == 1 && F == 1, tmax);
+    tmax = pass_bits<P::width(0), T>(lds, K, P::start(0), P::np == 1 && F == 1, tmax);
     __syncthreads();
   }
   if constexpr (P::np > 1) {
-    tmax = pass_bits<P::width(1)>(lds, K, P::start(1), P::np == 2 && F == 1, tmax);
+    tmax = pass_bits<P::width(1), T>(lds, K, P::start(1), P::np == 2 && F == 1, tmax);
     __syncthreads();
   }
   if constexpr (P::np > 2) {
-    tmax = pass_bits<P::width(2)>(lds, K, P::start(2), F == 1, tmax);
+    tmax = pass_bits<P::width(2), T>(lds, K, P::start(2), F == 1, tmax);
     __syncthreads();
   }
   if constexpr (F == 28) {
-    tmax = pass_28(lds, K, J, tmax);
+    tmax = pass_28<T>(lds, K, J, tmax);
     __syncthreads();
   }
 
@@ -220,7 +257,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
   __syncthreads();
   float amax = red[0];
 #pragma unroll
-  for (int w = 1; w < kThreads / 64; ++w) amax = fmaxf(amax, red[w]);
+  for (int w = 1; w < T / 64; ++w) amax = fmaxf(amax, red[w]);
 
   constexpr float qmax = (float)((1 << (BITS - 1)) - 1);
   const float sc = amax / qmax;                 // IEEE division
@@ -234,24 +271,18 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
     }
   }
 
-  for (int q = threadIdx.x; q < nchunk; q += kThreads) {
+  for (int q = threadIdx.x; q < nchunk; q += T) {
     const float4* src = reinterpret_cast<const float4*>(lds + lidx(q * 8));
     const float4 a = src[0], b = src[1];
     const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    uint32_t bt[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) bt[k] = round_bits(v[k], sc, rc);
     if (BITS == 4) {
-      uint32_t packed = 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        packed |= (uint32_t)(quantize_one<4>(v[k], sc, rc) & 0xF) << (4 * k);
-      reinterpret_cast<uint32_t*>(codes + (size_t)row * (K / 2))[q] = packed;
+      reinterpret_cast<uint32_t*>(codes + (size_t)row * (K / 2))[q] = pack_nibbles(bt);
     } else {
-      uint32_t lo = 0, hi = 0;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        lo |= (uint32_t)(quantize_one<8>(v[k], sc, rc) & 0xFF) << (8 * k);
-        hi |= (uint32_t)(quantize_one<8>(v[k + 4], sc, rc) & 0xFF) << (8 * k);
-      }
-      reinterpret_cast<uint2*>(codes + (size_t)row * K)[q] = make_uint2(lo, hi);
+      reinterpret_cast<uint2*>(codes + (size_t)row * K)[q] =
+          make_uint2(low_bytes(bt[0], bt[1], bt[2], bt[3]), low_bytes(bt[4], bt[5], bt[6], bt[7]));
     }
   }
 }
@@ -260,10 +291,10 @@ size_t lds_bytes(int K) {
   return (size_t)(K + ((K + 255) >> 8) * 8) * sizeof(float);
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J>
-hipError_t launch_one(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                      hipStream_t stream) {
-  auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J>;
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T>
+hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
+                        hipStream_t stream) {
+  auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T>;
   static bool attr_set = false;
   if (!attr_set) {
     // Rows above 64 KiB of LDS need the larger dynamic allocation enabled.
@@ -273,9 +304,20 @@ hipError_t launch_one(const Tin* x, int64_t M, int K, uint8_t* codes, float* sca
     (void)hipGetLastError();
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(kThreads), lds_bytes(K), stream, x, K,
+  hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(T), lds_bytes(K), stream, x, K,
                      codes, scales);
   return hipGetLastError();
+}
+
+// Few rows (decode): 1024 threads per row shorten each row's latency; many
+// rows: 256 threads, several rows per compute unit.
+constexpr int64_t kFewRows = 64;
+
+template <typename Tin, int BITS, bool WEIGHT, int F, int J>
+hipError_t launch_one(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
+                      hipStream_t stream) {
+  if (M <= kFewRows) return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024>(x, M, K, codes, scales, stream);
+  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads>(x, M, K, codes, scales, stream);
 }
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J = 0>
@@ -303,12 +345,6 @@ hipError_t dispatch_j(int j, const Tin* x, int64_t M, int K, uint8_t* codes, flo
 // of bank conflicts and their addresses are a per-thread base plus
 // compile-time offsets.  Phase 1 loads from global memory and the final pass
 // re-reads the phase-1 layout to quantize 16 consecutive elements per thread.
-//
-// Codes are rounded with the fp32 adder: t + 1.5 * 2^23 rounds t to the
-// nearest integer, ties to even, and leaves it in the low mantissa bits
-// (two's complement), from which nibbles and bytes are packed with byte
-// permutes and one bit-field insert.  |code| <= qmax holds without a clamp:
-// |t| <= fl32(amax / s) with s = fl32(amax / qmax) rounds to at most qmax.
 // ---------------------------------------------------------------------------
 constexpr int kSeg = 4096;
 constexpr int kSegFloats = kSeg + kSeg / 16;        // 4 floats of padding per 64
@@ -334,18 +370,6 @@ __device__ __forceinline__ void stages16(float* v) {
   }
 }
 
-__device__ __forceinline__ uint32_t round_bits(float y, float s, float r) {
-  const float q = y * r;
-  const float e = __builtin_fmaf(-q, s, y);
-  const float t = __builtin_fmaf(e, r, q);
-  return __float_as_uint(t + 12582912.0f);          // 1.5 * 2^23
-}
-// Low bytes of four words: [b0, b1, b2, b3].
-__device__ __forceinline__ uint32_t low_bytes(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
-  const uint32_t x01 = __builtin_amdgcn_perm(b1, b0, 0x0c0c0400u);
-  const uint32_t x23 = __builtin_amdgcn_perm(b3, b2, 0x0c0c0400u);
-  return __builtin_amdgcn_perm(x23, x01, 0x05040100u);
-}
 
 __device__ __forceinline__ float absmax16(const float* v, float m) {
 #pragma unroll
@@ -466,14 +490,7 @@ rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
     }
     const bool full = e + 8 < K;   // else only the first 8 elements are in the row
     if (BITS == 4) {
-      uint32_t w[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const uint32_t* b = bt + 8 * h;
-        const uint32_t ev = low_bytes(b[0], b[2], b[4], b[6]);
-        const uint32_t od = low_bytes(b[1], b[3], b[5], b[7]);
-        w[h] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
-      }
+      const uint32_t w[2] = {pack_nibbles(bt), pack_nibbles(bt + 8)};
       // Rows start 8-byte aligned when K % 32 == 0; otherwise word stores.
       uint32_t* dst = reinterpret_cast<uint32_t*>(codes + (size_t)row * (K / 2) + e / 2);
       if (full && K % 32 == 0) {
