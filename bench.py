@@ -132,45 +132,87 @@ def time_layer(torch, dptq, cfg, args):
     torch.cuda.synchronize()
 
     n_layers = 32
-    def step(i, ev=None):
+    def step(i):
         bits_all = dptq.layer_policy(n_layers)
         seq = (bits_all[n_layers // 2], bits_all[0])     # a non-sensitive, a sensitive layer
         r = i % R
-        k = 0
         for bits in seq:
-            if ev is not None:
-                ev[k].record()
             dptq.rotate_quant(xs[r], h, bits, codes[bits], scales)
-            if ev is not None:
-                ev[k + 1].record()
             dptq.qlinear(codes[bits], scales, bits, wps[r], wss[r], y)
-            k += 2
-        if ev is not None:
-            ev[k].record()
         return seq
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    evs = [_events(torch, 5) for _ in range(args.steps)]
+    e0, e1 = _events(torch, 2)
     t0 = time.perf_counter()
+    e0.record()
     for i in range(args.steps):
-        seq = step(i, evs[i])
+        seq = step(i)
+    e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    # per-kernel durations (events bracket each launch on its stream)
-    names = [f"rotate_quant_a{seq[0]}", f"gemm_a{seq[0]}", f"rotate_quant_a{seq[1]}",
-             f"gemm_a{seq[1]}"]
-    per = {n: 0.0 for n in names}
-    for ev in evs:
-        for k, n in enumerate(names):
-            per[n] += ev[k].elapsed_time(ev[k + 1])
-    per = {n: v / args.steps for n, v in per.items()}
-    return wall, per, seq
+    gpu_ms = e0.elapsed_time(e1)
+    return wall, gpu_ms, seq
+
+
+def time_kernels(torch, dptq, cfg, args, seq, reps=24):
+    """Average duration (ms) of each kernel of the step, from `reps`
+    back-to-back launches captured in a HIP graph and replayed between two HIP
+    events on the launch stream (no host launch gaps, no events between the
+    launches).  Inputs cycle over the same copies as the step."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
+    rng = np.random.default_rng(cfg["seed"] + 7)
+    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
+    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
+    wp, ws = dptq.prepare_weights(w, h)
+    del w
+    R = max(1, args.copies)
+    xs = [x.clone() for _ in range(R)]
+    wps = [wp.clone() for _ in range(R)]
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    out = {}
+    for bits in seq:
+        codes, scales = dptq.rotate_quant(x, h, bits)
+        out[f"gemm_a{bits}"] = _graph_time(torch, [
+            (lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
+            for i in range(reps)]) / 1e3
+        out[f"rotate_quant_a{bits}"] = _graph_time(torch, [
+            (lambda i: (lambda: dptq.rotate_quant(xs[i % R], h, bits, codes, scales)))(i)
+            for i in range(reps)]) / 1e3
+    return out
+
+
+def _graph_time(torch, fns, reps=5):
+    """Microseconds per call of a sequence of launches, captured once in a HIP
+    graph and replayed (no host launch gaps)."""
+    for f in fns:
+        f()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=s):
+        for f in fns:
+            f()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = _events(torch, 2)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (reps * len(fns))
 
 
 def time_decode(torch, dptq, args):
-    """Weight-streaming GB/s on the LLaMA-3-8B down_proj decode shapes."""
+    """Decode shapes of the LLaMA-3-8B down projection (K = 14336, N = 4096,
+    h = 28 x 512): GEMM GB/s and rotate+quantize latency, each as graph-replayed
+    back-to-back launches cycling 12 weight copies (more than the 256 MiB
+    last-level cache holds)."""
     import numpy as np
     import workloads
     dev = torch.device("cuda:0")
@@ -187,26 +229,13 @@ def time_decode(torch, dptq, args):
         for bits in (4, 8):
             codes, scales = dptq.rotate_quant(x, h, bits)
             y = torch.empty((M, N), dtype=torch.float16, device=dev)
-            for i in range(5):
-                dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)
-            reps = 60
-            e0, e1 = _events(torch, 2)
-            e0.record()
-            for i in range(reps):
-                dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)
-            e1.record()
-            torch.cuda.synchronize()
-            us = e0.elapsed_time(e1) * 1e3 / reps
+            us = _graph_time(torch, [
+                (lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
+                for i in range(24)])
             nbytes = N * K // 2 + 4 * N + M * K * bits // 8 + 4 * M + 2 * M * N
-            out[f"decode_M{M}_a{bits}"] = {"us": round(us, 2),
-                                           "GB/s": round(nbytes / us / 1e3, 1)}
-            e0, e1 = _events(torch, 2)
-            e0.record()
-            for i in range(reps):
-                dptq.rotate_quant(x, h, bits, codes, scales)
-            e1.record()
-            torch.cuda.synchronize()
-            out[f"rotate_quant_M{M}_a{bits}_us"] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+            out[f"decode_M{M}_a{bits}"] = {"us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
+            us_rq = _graph_time(torch, [lambda: dptq.rotate_quant(x, h, bits, codes, scales)] * 24)
+            out[f"rotate_quant_M{M}_a{bits}_us"] = round(us_rq, 2)
     return out
 
 
@@ -257,15 +286,17 @@ def main():
         run_only(torch, dptq, cfg, args)
         return
 
-    wall, per, seq = time_layer(torch, dptq, cfg, args)
+    wall, gpu_ms, seq = time_layer(torch, dptq, cfg, args)
     ops_gemm = 2.0 * M * N * K
     ops_step = ops_gemm * len(seq)
     value = ops_step * args.steps / wall / 1e12
     ms_step = wall * 1e3 / args.steps
 
+    per = time_kernels(torch, dptq, cfg, args, seq)
     gemm_a4_ms = per[f"gemm_a{seq[0]}"]
     achieved = ops_gemm / (gemm_a4_ms * 1e-3) / 1e12
     k1_bytes = 2 * M * K + M * K * 4 // 8 + 4 * M
+    rq4_ms = per[f"rotate_quant_a{seq[0]}"]
     rec = {
         "metric": METRIC, "value": round(value, 3), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
@@ -274,12 +305,14 @@ def main():
         "config": {"workload": "llama2-7b fused qkv qlinear, rotate+quant+GEMM at A4 then A8",
                    "M": M, "K": K, "N": N, "had_size": cfg["h"], "bits": list(seq),
                    "parallelism": "none"},
-        "roofline": {"bound": "mfma", "kernel": "qgemm_prefill<4>",
+        "roofline": {"bound": "mfma", "kernel": "qgemm_prefill_wide<4>",
                      "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
                      "traffic": measured_traffic()},
+        "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
-        "rotate_quant_a4_GBs": round(k1_bytes / (per[f"rotate_quant_a{seq[0]}"] * 1e-3) / 1e9, 1),
+        "rotate_quant_a4": {"bound": "alu", "GB/s": round(k1_bytes / (rq4_ms * 1e-3) / 1e9, 1),
+                            "frac_of_hbm_peak": round(k1_bytes / (rq4_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
     }
     if args.extended:
         rec["decode"] = time_decode(torch, dptq, args)
