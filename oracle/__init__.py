@@ -19,6 +19,8 @@ Modules
   gemm      exact integer GEMM and the per-token x per-channel dequant epilogue
             (Section 2, Y = X W^T).
   policy    phase-aware activation bit policy (Eq. 21, Algorithm 1 step 2).
+  residual  Jump Ratio, Historical Feature SNR and the sensitive-layer rule
+            (Section 3.1 Eq. 8-11, Section 3.3 Eq. 20).
 """
 
 from .hadamard import (sylvester, paley28, hadamard, split_had_size,
@@ -27,6 +29,8 @@ from .quant import (qmax_for_bits, quantize_rows, pack_int4, unpack_int4,
                     rotate_quant_ref, prepare_weights_ref, dequant_rows)
 from .gemm import qlinear_acc_ref, qlinear_acc_entries, epilogue_ref, qlinear_ref
 from .policy import layer_policy_ref
+from .residual import (jump_ratio_tokens_ref, inverse_rotate_f64, reconstructed_history_ref,
+                       hist_snr_tokens_ref, residual_dynamics_ref, select_sensitive_layers_ref)
 
 __all__ = [
     "sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows",
@@ -34,4 +38,6 @@ __all__ = [
     "rotate_quant_ref", "prepare_weights_ref", "dequant_rows",
     "qlinear_acc_ref", "qlinear_acc_entries", "epilogue_ref", "qlinear_ref",
     "layer_policy_ref",
+    "jump_ratio_tokens_ref", "inverse_rotate_f64", "reconstructed_history_ref",
+    "hist_snr_tokens_ref", "residual_dynamics_ref", "select_sensitive_layers_ref",
 ]

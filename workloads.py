@@ -18,7 +18,7 @@ shapes and value structure:
 import numpy as np
 
 __all__ = ["CONFIGS", "gauss_massive", "gauss_outliers", "student_t",
-           "residual_phase", "weights", "layer_mask", "activations_for"]
+           "residual_phase", "residual_stream", "weights", "layer_mask", "activations_for"]
 
 # name -> description.  Linear tuples are (name, K, N, had_size).
 CONFIGS = {
@@ -93,6 +93,34 @@ def residual_phase_plan(rng, K, L):
     factors = [(float(rng.uniform(100, 1000)), float(rng.uniform(10, 50)))
                for _ in range(n)]
     return (p1, p2), channels, factors
+
+
+def residual_stream(rng, L, T, d, n_massive=3, early=3):
+    """Per-layer (x, dx) pairs, fp16 [T, d] each, of a synthetic residual stream
+    x^(l+1) = x^(l) + dx^(l) with the three-phase depth pattern of Section 2:
+    in the first `early` layers massive activations emerge (large updates on a
+    few seeded channels, largest on token 0, plus updates of the stream's own
+    size); in the middle layers the updates are small relative to the stream;
+    the last layer redistributes the massive channels with another large
+    update.  The states are kept in fp32 and handed out rounded to fp16."""
+    x = (0.5 * rng.standard_normal((T, d))).astype(np.float32)
+    channels = rng.choice(d, n_massive, replace=False)
+    out = []
+    for layer in range(L):
+        scale = float(np.sqrt(np.mean(x.astype(np.float64) ** 2)))
+        if layer < early:
+            dx = (2.0 * scale) * rng.standard_normal((T, d))
+            dx[:, channels] += rng.uniform(20, 60, size=n_massive) * scale
+            dx[0, channels] += rng.uniform(100, 300, size=n_massive) * scale
+        elif layer == L - 1:
+            dx = (2.0 * scale) * rng.standard_normal((T, d))
+            dx[:, channels] -= 0.9 * x[:, channels]
+        else:
+            dx = (0.05 * scale) * rng.standard_normal((T, d))
+        dx = dx.astype(np.float32)
+        out.append((_to_f16(x), _to_f16(dx)))
+        x = x + dx
+    return out
 
 
 def weights(rng, N, K, std=0.02):
