@@ -139,6 +139,47 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
                         int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream);
 
 /*
+ * dptq_residual_dynamics - residual-dynamics calibration statistics of one
+ * layer (Section 3.1 Eq. 8-11; quantization in the rotated space, Section 3.2
+ * Eq. 14-16).  For every token row t of the residual state x entering the
+ * layer and the update dx the layer adds:
+ *
+ *   jr[t]  = ||dx_t||_2 / (||x_t||_2 + eps)                       (Eq. 8)
+ *   snr[t] = 10 log10(||x_t||^2 / (||xhat_t - x_t||^2 + eps))      (Eq. 11)
+ *
+ * with xhat_t = Q_b(x_t + dx_t) - dx_t (Eq. 10), where Q_b is the path's own
+ * quantizer: u = fl32(x + dx) rotated by I (x) H_h exactly as
+ * dptq_rotate_quant rotates, quantized per token at `bits`, and mapped back by
+ * the inverse rotation.  The error energy is taken in the rotated space and
+ * divided by h, which equals ||Q_b(u) - u||^2 for the unnormalized H_h.
+ * Norms and error energy accumulate in fp32 (any order), the final
+ * arithmetic is fp64; results agree with an fp64 evaluation to about 1e-5
+ * relative (JR) and 1e-4 dB (SNR).
+ *
+ *   x, dx       device, fp16 [T, K], row-major, 16-byte aligned
+ *   T, K, had_size   as for dptq_rotate_quant
+ *   bits        4 or 8: the activation precision whose damage is measured
+ *   eps         >= 0, finite (the eps of Eq. 8 and 11; the paper gives no value)
+ *   jr, snr     device, float [T] outputs
+ *   layer_means device, double [2] output {mean jr, mean snr} (Eq. 9 and the
+ *               layer value of Eq. 11), or NULL to skip
+ *
+ * T = 0 enqueues nothing.
+ */
+int dptq_residual_dynamics(const void* x, const void* dx, int64_t T, int64_t K, int32_t had_size,
+                           int32_t bits, float eps, float* jr, float* snr, double* layer_means,
+                           void* stream);
+
+/*
+ * dptq_select_layers - the sensitive-layer rule of Eq. 20 (host only):
+ * bits_out[l] = 8 if jr[l] > tau_jr and snr[l] < tau_snr, else 4, for the
+ * layer statistics jr[l], snr[l] (host arrays [num_layers], e.g. the layer
+ * means of dptq_residual_dynamics).  The paper gives no threshold values.
+ */
+int dptq_select_layers(int32_t num_layers, const double* jr, const double* snr, double tau_jr,
+                       double tau_snr, int32_t* bits_out);
+
+/*
  * dptq_layer_policy - phase-aware activation precision (host only).
  * Algorithm 1 step 2 with the sensitive set of Eq. 21.
  *

@@ -83,7 +83,8 @@ def hist_snr_tokens_ref(x, dx, had_size, bits=4, eps=DEFAULT_EPS):
     num = np.sum(x64 * x64, axis=1)
     err = xhat - x64
     den = np.sum(err * err, axis=1) + eps
-    return 10.0 * np.log10(num / den)
+    with np.errstate(divide="ignore"):       # a zero history has SNR -inf
+        return 10.0 * np.log10(num / den)
 
 
 def residual_dynamics_ref(x, dx, had_size, bits=4, eps=DEFAULT_EPS):

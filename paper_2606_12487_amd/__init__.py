@@ -15,7 +15,8 @@ import ctypes
 import os
 
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
-           "layer_policy", "prepare_weights", "version", "EXPORTED_FUNCTIONS", "GEMM_AUTO",
+           "layer_policy", "prepare_weights", "residual_dynamics", "select_layers", "version",
+           "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
 _PKG_DIR = os.path.dirname(os.path.abspath(__file__))
@@ -25,6 +26,7 @@ _lib = None
 # Every function the C ABI exports (include/dptq.h).
 EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_qlinear", "dptq_qlinear_acc", "dptq_qlinear_kernel",
+                      "dptq_residual_dynamics", "dptq_select_layers",
                       "dptq_layer_policy", "dptq_prepare_weights")
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
@@ -64,6 +66,11 @@ def lib():
         L.dptq_qlinear_acc.restype = ctypes.c_int
         L.dptq_qlinear_kernel.argtypes = [vp, vp, i64, i64, i32, vp, vp, i64, vp, vp, i32, vp]
         L.dptq_qlinear_kernel.restype = ctypes.c_int
+        L.dptq_residual_dynamics.argtypes = [vp, vp, i64, i64, i32, i32, ctypes.c_float,
+                                             vp, vp, vp, vp]
+        L.dptq_residual_dynamics.restype = ctypes.c_int
+        L.dptq_select_layers.argtypes = [i32, vp, vp, ctypes.c_double, ctypes.c_double, vp]
+        L.dptq_select_layers.restype = ctypes.c_int
         L.dptq_layer_policy.argtypes = [i32, vp, vp]
         L.dptq_layer_policy.restype = ctypes.c_int
         L.dptq_prepare_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp]
@@ -191,6 +198,50 @@ def qlinear_acc(codes, bits, w_packed, acc=None, kernel=GEMM_AUTO):
                                          N, None, _ptr(acc), int(kernel), _stream(codes)),
                "dptq_qlinear_kernel")
     return acc
+
+
+def residual_dynamics(x, dx, had_size, bits=4, eps=1e-8, jr=None, snr=None, means=None):
+    """One layer's residual-dynamics statistics (Eq. 8-11): per-token Jump Ratio
+    and historical SNR (dB) of the updates dx added to the states x (both fp16
+    [T, K]), measured through the rotated `bits`-bit quantizer; returns
+    (jr float32 [T], snr float32 [T], means float64 [2] = layer JR, layer SNR)."""
+    torch = _torch()
+    _require(x, "x", torch.float16)
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [T, K]")
+    T, K = x.shape
+    _require(dx, "dx", torch.float16, (T, K))
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    if jr is None:
+        jr = torch.empty((T,), dtype=torch.float32, device=x.device)
+    if snr is None:
+        snr = torch.empty((T,), dtype=torch.float32, device=x.device)
+    if means is None:
+        means = torch.empty((2,), dtype=torch.float64, device=x.device)
+    _require(jr, "jr", torch.float32, (T,))
+    _require(snr, "snr", torch.float32, (T,))
+    _require(means, "means", torch.float64, (2,))
+    _check(lib().dptq_residual_dynamics(_ptr(x), _ptr(dx), T, K, int(had_size), int(bits),
+                                        float(eps), _ptr(jr), _ptr(snr), _ptr(means),
+                                        _stream(x)), "dptq_residual_dynamics")
+    return jr, snr, means
+
+
+def select_layers(jr_layers, snr_layers, tau_jr, tau_snr):
+    """Activation bits per layer by the sensitive-layer rule of Eq. 20."""
+    jr = [float(v) for v in jr_layers]
+    snr = [float(v) for v in snr_layers]
+    if len(jr) != len(snr) or not jr:
+        raise ValueError("one JR and one SNR value per layer, at least one layer")
+    L = len(jr)
+    a = (ctypes.c_double * L)(*jr)
+    b = (ctypes.c_double * L)(*snr)
+    out = (ctypes.c_int32 * L)()
+    _check(lib().dptq_select_layers(L, ctypes.cast(a, ctypes.c_void_p), ctypes.cast(b, ctypes.c_void_p),
+                                    float(tau_jr), float(tau_snr), ctypes.cast(out, ctypes.c_void_p)),
+           "dptq_select_layers")
+    return list(out)
 
 
 def layer_policy(num_layers, mask=None):

@@ -106,6 +106,32 @@ int dptq_qlinear_acc(const void* codes, int64_t M, int64_t K, int32_t bits,
                                        nullptr, acc, dptq::kGemmAuto, static_cast<hipStream_t>(stream)));
 }
 
+int dptq_residual_dynamics(const void* x, const void* dx, int64_t T, int64_t K, int32_t had_size,
+                           int32_t bits, float eps, float* jr, float* snr, double* layer_means,
+                           void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(T, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (bits != 4 && bits != 8) return DPTQ_ERR_INVALID_ARG;
+  if (!(eps >= 0.0f) || eps > 3.0e38f) return DPTQ_ERR_INVALID_ARG;   // also rejects NaN
+  if (T == 0) return DPTQ_OK;
+  if (!x || !dx || !jr || !snr) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(dx)) return DPTQ_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(jr) & 3u) || (reinterpret_cast<uintptr_t>(snr) & 3u) ||
+      (reinterpret_cast<uintptr_t>(layer_means) & 7u))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_residual_stats(x, dx, T, (int)K, hs, bits, eps, jr, snr,
+                                              layer_means, static_cast<hipStream_t>(stream)));
+}
+
+int dptq_select_layers(int32_t num_layers, const double* jr, const double* snr, double tau_jr,
+                       double tau_snr, int32_t* bits_out) {
+  if (num_layers < 1 || !jr || !snr || !bits_out) return DPTQ_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < num_layers; ++l)
+    bits_out[l] = (jr[l] > tau_jr && snr[l] < tau_snr) ? 8 : 4;
+  return DPTQ_OK;
+}
+
 int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int64_t K,
                         int32_t bits, const uint8_t* w_packed, const float* w_scales,
                         int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream) {

@@ -23,6 +23,13 @@ hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
 hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
                                   uint8_t* w_packed, float* w_scales,
                                   hipStream_t stream);
+// Residual-dynamics statistics of x + dx (statistics mode of the rotate+quantize
+// kernels): per-row Jump Ratio and historical SNR (dB), and their means when
+// means != nullptr.
+hipError_t launch_residual_stats(const void* x, const void* dx, int64_t T, int K, HadSplit hs,
+                                 int bits, float eps, float* jr, float* snr, double* means,
+                                 hipStream_t stream);
+
 // GEMM kernels (values of dptq_gemm_kernel).
 constexpr int kGemmAuto = 0, kGemmDecode = 1, kGemmTile = 2, kGemmWide = 3;
 

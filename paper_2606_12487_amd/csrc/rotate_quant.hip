@@ -99,6 +99,7 @@ __device__ __forceinline__ float absmax8(const float* v, float m) {
   return m;
 }
 
+
 // One pass over index bits [s, s+G): each work item gathers the 2^G elements
 // that differ only in those bits, applies the butterflies, and writes back.
 template <int G, int T>
@@ -192,6 +193,78 @@ __device__ __forceinline__ uint32_t pack_nibbles(const uint32_t* b) {
   return (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
 }
 
+// Statistics mode (residual-dynamics calibration, Section 3.1): the kernels
+// rotate and quantize u = fl32(x + dx) and, instead of codes, write per row
+// the Jump Ratio ||dx|| / (||x|| + eps) and the historical SNR
+// 10 log10(||x||^2 / (||Q(u) - u||^2 + eps)), where ||Q(u) - u||^2 is the
+// rotated-space error energy over h (Eq. 16 with the unnormalized B_h).
+struct StatsArgs {
+  const __half* dx;   // [M, K] updates (nullptr in codes mode)
+  float* jr;          // [M]
+  float* snr;         // [M], dB
+  float eps;
+};
+
+// Eight elements of x and dx: v = fl32(x + dx), and the squared norms.
+__device__ __forceinline__ void load8_sum(const __half* x, const __half* d, float* v,
+                                          float& sx, float& sd) {
+  float b[8];
+  load8(x, v);
+  load8(d, b);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    sx = __builtin_fmaf(v[k], v[k], sx);
+    sd = __builtin_fmaf(b[k], b[k], sd);
+    v[k] = v[k] + b[k];
+  }
+}
+
+// Sum over the workgroup, in a fixed order (wavefront butterflies, then the
+// wavefronts in order); every thread gets the result.
+template <int T>
+__device__ __forceinline__ float3 block_sum3(float3 a, float (*red)[3]) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a.x += __shfl_xor(a.x, off);
+    a.y += __shfl_xor(a.y, off);
+    a.z += __shfl_xor(a.z, off);
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6][0] = a.x;
+    red[threadIdx.x >> 6][1] = a.y;
+    red[threadIdx.x >> 6][2] = a.z;
+  }
+  __syncthreads();
+  float3 r = make_float3(red[0][0], red[0][1], red[0][2]);
+#pragma unroll
+  for (int w = 1; w < T / 64; ++w) {
+    r.x += red[w][0];
+    r.y += red[w][1];
+    r.z += red[w][2];
+  }
+  return r;
+}
+
+// Error energy of quantizing v[0..n) with scale s (reciprocal r).
+template <int N>
+__device__ __forceinline__ float quant_error_energy(const float* v, float s, float r, float ee) {
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const int code = (int)(round_bits(v[k], s, r) - 0x4B400000u);
+    const float e = __builtin_fmaf((float)code, s, -v[k]);
+    ee = __builtin_fmaf(e, e, ee);
+  }
+  return ee;
+}
+
+// JR and SNR of one row from ||x||^2, ||dx||^2 and the rotated error energy.
+__device__ __forceinline__ void write_stats(const StatsArgs& st, int row, float3 sums, int h) {
+  const double sx = sums.x, sd = sums.y, ee = sums.z;
+  st.jr[row] = (float)(sqrt(sd) / (sqrt(sx) + (double)st.eps));
+  st.snr[row] = (float)(10.0 * log10(sx / (ee / h + (double)st.eps)));
+}
+
 // Compile-time pass plan for h = F * 2^J: the load pass covers index bits
 // 0 .. min(J, 3) - 1, the remaining power-of-two bits are split as evenly as
 // possible into at most three passes of at most 5 bits.
@@ -208,12 +281,14 @@ struct Plan {
   static constexpr int width_from(int s, int left) { return (J - s + left - 1) / left; }
 };
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T>
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS>
 __global__ void __launch_bounds__(T)
 rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
-                    float* __restrict__ scales) {
+                    float* __restrict__ scales, StatsArgs st) {
   extern __shared__ float lds[];
   __shared__ float red[T / 64];
+  __shared__ float red3[T / 64][3];
+  float3 sums = make_float3(0.0f, 0.0f, 0.0f);
   using P = Plan<J>;
   static_assert(P::np <= 3, "pass plan too long");
   const int row = blockIdx.x;
@@ -224,7 +299,8 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
   float tmax = 0.0f;
   for (int q = threadIdx.x; q < nchunk; q += T) {
     float v[8];
-    load8(xr + (size_t)q * 8, v);
+    if constexpr (STATS) load8_sum(xr + (size_t)q * 8, st.dx + (size_t)row * K + (size_t)q * 8, v, sums.x, sums.y);
+    else load8(xr + (size_t)q * 8, v);
     butterflies<3>(v, 0, P::j0);
     if (load_last) tmax = absmax8(v, tmax);
     float4* d = reinterpret_cast<float4*>(lds + lidx(q * 8));
@@ -262,7 +338,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
   constexpr float qmax = (float)((1 << (BITS - 1)) - 1);
   const float sc = amax / qmax;                 // IEEE division
   const float rc = sc != 0.0f ? 1.0f / sc : 0.0f;
-  if (threadIdx.x == 0) {
+  if (!STATS && threadIdx.x == 0) {
     if (WEIGHT) {
       constexpr int h = F << J;
       scales[row] = sc / (float)h;              // fold the 1/h of the rotation
@@ -275,6 +351,10 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
     const float4* src = reinterpret_cast<const float4*>(lds + lidx(q * 8));
     const float4 a = src[0], b = src[1];
     const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    if constexpr (STATS) {
+      sums.z = quant_error_energy<8>(v, sc, rc, sums.z);
+      continue;
+    }
     uint32_t bt[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) bt[k] = round_bits(v[k], sc, rc);
@@ -285,16 +365,20 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
           make_uint2(low_bytes(bt[0], bt[1], bt[2], bt[3]), low_bytes(bt[4], bt[5], bt[6], bt[7]));
     }
   }
+  if constexpr (STATS) {
+    sums = block_sum3<T>(sums, red3);
+    if (threadIdx.x == 0) write_stats(st, row, sums, F << J);
+  }
 }
 
 size_t lds_bytes(int K) {
   return (size_t)(K + ((K + 255) >> 8) * 8) * sizeof(float);
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T>
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS>
 hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                        hipStream_t stream) {
-  auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T>;
+                        StatsArgs st, hipStream_t stream) {
+  auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T, STATS>;
   static bool attr_set = false;
   if (!attr_set) {
     // Rows above 64 KiB of LDS need the larger dynamic allocation enabled.
@@ -305,7 +389,7 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* s
     attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(T), lds_bytes(K), stream, x, K,
-                     codes, scales);
+                     codes, scales, st);
   return hipGetLastError();
 }
 
@@ -313,22 +397,23 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* s
 // rows: 256 threads, several rows per compute unit.
 constexpr int64_t kFewRows = 64;
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J>
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS>
 hipError_t launch_one(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                      hipStream_t stream) {
-  if (M <= kFewRows) return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024>(x, M, K, codes, scales, stream);
-  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads>(x, M, K, codes, scales, stream);
+                      StatsArgs st, hipStream_t stream) {
+  if (M <= kFewRows)
+    return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS>(x, M, K, codes, scales, st, stream);
+  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS>(x, M, K, codes, scales, st, stream);
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J = 0>
+template <typename Tin, int BITS, bool WEIGHT, int F, bool STATS, int J = 0>
 hipError_t dispatch_j(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                      hipStream_t stream) {
+                      StatsArgs st, hipStream_t stream) {
   constexpr int kMaxJ = F == 1 ? 15 : 10;   // h <= 32768
   if constexpr (J > kMaxJ) {
     return hipErrorInvalidValue;
   } else {
-    if (j == J) return launch_one<Tin, BITS, WEIGHT, F, J>(x, M, K, codes, scales, stream);
-    return dispatch_j<Tin, BITS, WEIGHT, F, J + 1>(j, x, M, K, codes, scales, stream);
+    if (j == J) return launch_one<Tin, BITS, WEIGHT, F, J, STATS>(x, M, K, codes, scales, st, stream);
+    return dispatch_j<Tin, BITS, WEIGHT, F, STATS, J + 1>(j, x, M, K, codes, scales, st, stream);
   }
 }
 
@@ -391,13 +476,15 @@ __device__ __forceinline__ float wave_max_nonneg(float m) {
   return __int_as_float(max(max(r0, r1), max(r2, r3)));
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int J>
+template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS>
 __global__ void __launch_bounds__(kThreads)
 rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
-               float* __restrict__ scales) {
+               float* __restrict__ scales, StatsArgs st) {
   static_assert(J <= 12, "segments hold 4096 elements");
   extern __shared__ float lds[];
   __shared__ float red[kThreads / 64];
+  __shared__ float red3[kThreads / 64][3];
+  float3 sums = make_float3(0.0f, 0.0f, 0.0f);
   const int row = blockIdx.x;
   const int t = threadIdx.x;
   const int nseg = (K + kSeg - 1) / kSeg;
@@ -414,14 +501,17 @@ rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
     const int e = sg * kSeg + 16 * t;
     // K is a multiple of 8: a thread's second 8 elements may lie past the
     // row end (then h <= 8 and they form blocks of their own).
+    const __half* dr = STATS ? st.dx + (size_t)row * K : nullptr;
     if (e < K) {
-      load8(xr + e, v);
+      if constexpr (STATS) load8_sum(xr + e, dr + e, v, sums.x, sums.y);
+      else load8(xr + e, v);
     } else {
 #pragma unroll
       for (int r = 0; r < 8; ++r) v[r] = 0.0f;
     }
     if (e + 8 < K) {
-      load8(xr + e + 8, v + 8);
+      if constexpr (STATS) load8_sum(xr + e + 8, dr + e + 8, v + 8, sums.x, sums.y);
+      else load8(xr + e + 8, v + 8);
     } else {
 #pragma unroll
       for (int r = 8; r < 16; ++r) v[r] = 0.0f;
@@ -473,7 +563,23 @@ rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
   constexpr float qmax = (float)((1 << (BITS - 1)) - 1);
   const float sc = amax / qmax;                 // IEEE division
   const float rc = sc != 0.0f ? 1.0f / sc : 0.0f;
-  if (t == 0) scales[row] = WEIGHT ? sc / (float)(1 << J) : sc;
+  if (!STATS && t == 0) scales[row] = WEIGHT ? sc / (float)(1 << J) : sc;
+
+  if constexpr (STATS) {
+    // Padding elements are zero and quantize to zero without error.
+    for (int sg = 0; sg < nseg; ++sg) {
+      const float* sl = lds + sg * kSegFloats + b1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 w4 = *reinterpret_cast<const float4*>(sl + 4 * q);
+        const float w[4] = {w4.x, w4.y, w4.z, w4.w};
+        sums.z = quant_error_energy<4>(w, sc, rc, sums.z);
+      }
+    }
+    sums = block_sum3<kThreads>(sums, red3);
+    if (t == 0) write_stats(st, row, sums, 1 << J);
+    return;
+  }
 
   for (int sg = 0; sg < nseg; ++sg) {
     const int e = sg * kSeg + 16 * t;
@@ -519,10 +625,10 @@ rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
 
 size_t pow2_lds_bytes(int K) { return (size_t)((K + kSeg - 1) / kSeg) * kSegFloats * sizeof(float); }
 
-template <typename Tin, int BITS, bool WEIGHT, int J>
+template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS>
 hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                       hipStream_t stream) {
-  auto kern = rq_pow2_kernel<Tin, BITS, WEIGHT, J>;
+                       StatsArgs st, hipStream_t stream) {
+  auto kern = rq_pow2_kernel<Tin, BITS, WEIGHT, J, STATS>;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -532,29 +638,56 @@ hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* sc
     attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(kThreads), pow2_lds_bytes(K), stream, x, K,
-                     codes, scales);
+                     codes, scales, st);
   return hipGetLastError();
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int J = 0>
+template <typename Tin, int BITS, bool WEIGHT, bool STATS, int J = 0>
 hipError_t dispatch_pow2(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                         hipStream_t stream) {
+                         StatsArgs st, hipStream_t stream) {
   if constexpr (J > 12) {
     return hipErrorInvalidValue;
   } else {
-    if (j == J) return launch_pow2<Tin, BITS, WEIGHT, J>(x, M, K, codes, scales, stream);
-    return dispatch_pow2<Tin, BITS, WEIGHT, J + 1>(j, x, M, K, codes, scales, stream);
+    if (j == J) return launch_pow2<Tin, BITS, WEIGHT, J, STATS>(x, M, K, codes, scales, st, stream);
+    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, J + 1>(j, x, M, K, codes, scales, st, stream);
   }
 }
 
-template <typename Tin, int BITS, bool WEIGHT>
+template <typename Tin, int BITS, bool WEIGHT, bool STATS = false>
 hipError_t launch_rq(const Tin* x, int64_t M, int K, HadSplit hs, uint8_t* codes,
-                     float* scales, hipStream_t stream) {
+                     float* scales, hipStream_t stream, StatsArgs st = StatsArgs{}) {
   if (M == 0) return hipSuccess;
-  if (hs.f == 28) return dispatch_j<Tin, BITS, WEIGHT, 28>(hs.j, x, M, K, codes, scales, stream);
+  if (hs.f == 28) return dispatch_j<Tin, BITS, WEIGHT, 28, STATS>(hs.j, x, M, K, codes, scales, st, stream);
   // Up to 4096 the register-phase kernel; larger sizes the general one.
-  if (hs.j <= 12) return dispatch_pow2<Tin, BITS, WEIGHT>(hs.j, x, M, K, codes, scales, stream);
-  return dispatch_j<Tin, BITS, WEIGHT, 1>(hs.j, x, M, K, codes, scales, stream);
+  if (hs.j <= 12) return dispatch_pow2<Tin, BITS, WEIGHT, STATS>(hs.j, x, M, K, codes, scales, st, stream);
+  return dispatch_j<Tin, BITS, WEIGHT, 1, STATS>(hs.j, x, M, K, codes, scales, st, stream);
+}
+
+// Layer means of the per-token statistics (Eq. 9 and Eq. 11): one workgroup
+// sums in fp64 in a fixed order.
+__global__ void __launch_bounds__(256)
+layer_means_kernel(const float* __restrict__ jr, const float* __restrict__ snr, int64_t T,
+                   double* __restrict__ out) {
+  __shared__ double red[2][256];
+  double a = 0.0, b = 0.0;
+  for (int64_t i = threadIdx.x; i < T; i += 256) {
+    a += (double)jr[i];
+    b += (double)snr[i];
+  }
+  red[0][threadIdx.x] = a;
+  red[1][threadIdx.x] = b;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + w];
+      red[1][threadIdx.x] += red[1][threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    out[0] = red[0][0] / (double)T;
+    out[1] = red[1][0] / (double)T;
+  }
 }
 
 }  // namespace
@@ -572,6 +705,20 @@ hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
                                   uint8_t* w_packed, float* w_scales,
                                   hipStream_t stream) {
   return launch_rq<float, 4, true>(w, N, K, hs, w_packed, w_scales, stream);
+}
+
+hipError_t launch_residual_stats(const void* x, const void* dx, int64_t T, int K, HadSplit hs,
+                                 int bits, float eps, float* jr, float* snr, double* means,
+                                 hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  const __half* xh = static_cast<const __half*>(x);
+  const StatsArgs st{static_cast<const __half*>(dx), jr, snr, eps};
+  const hipError_t e =
+      bits == 4 ? launch_rq<__half, 4, false, true>(xh, T, K, hs, nullptr, nullptr, stream, st)
+                : launch_rq<__half, 8, false, true>(xh, T, K, hs, nullptr, nullptr, stream, st);
+  if (e != hipSuccess || means == nullptr) return e;
+  hipLaunchKernelGGL(layer_means_kernel, dim3(1), dim3(256), 0, stream, jr, snr, T, means);
+  return hipGetLastError();
 }
 
 }  // namespace dptq

@@ -148,6 +148,40 @@ def test_qlinear_kernel_validation(L):
     assert qk(L, M=0, kernel=dptq.GEMM_DECODE, codes=NULL, a_s=NULL, w=NULL, w_s=NULL) == OK
 
 
+def rd(L, x=FAKE, dx=FAKE, T=4, K=256, h=256, bits=4, eps=1e-8, jr=FAKE, snr=FAKE, means=FAKE):
+    return L.dptq_residual_dynamics(x, dx, T, K, h, bits, eps, jr, snr, means, NULL)
+
+
+def test_residual_dynamics_validation(L):
+    assert rd(L, bits=3) == INVALID
+    assert rd(L, h=12) == INVALID
+    assert rd(L, K=384) == INVALID               # h does not divide K
+    assert rd(L, K=36864 + 256) == UNSUPPORTED
+    assert rd(L, eps=-1.0) == INVALID
+    assert rd(L, eps=float("nan")) == INVALID
+    assert rd(L, eps=float("inf")) == INVALID
+    for name in ("x", "dx", "jr", "snr"):
+        assert rd(L, **{name: NULL}) == INVALID, name
+    assert rd(L, x=MISALIGNED) == INVALID
+    assert rd(L, dx=MISALIGNED) == INVALID
+    assert rd(L, means=ctypes.c_void_p(0x10004)) == INVALID    # doubles need 8-byte alignment
+    assert rd(L, T=0, x=NULL, dx=NULL, jr=NULL, snr=NULL, means=NULL) == OK
+
+
+def test_select_layers_matches_oracle(L):
+    import random
+    from oracle.residual import select_sensitive_layers_ref
+    rnd = random.Random(7)
+    for _ in range(50):
+        n = rnd.randint(1, 40)
+        jr = [rnd.choice([0.1, 0.5, 0.9, rnd.random()]) for _ in range(n)]
+        snr = [rnd.choice([5.0, 15.0, 25.0, 30 * rnd.random()]) for _ in range(n)]
+        tj, ts = rnd.choice([0.5, 0.3]), rnd.choice([15.0, 20.0])
+        assert dptq.select_layers(jr, snr, tj, ts) == select_sensitive_layers_ref(jr, snr, tj, ts)[1]
+    out = (ctypes.c_int32 * 2)()
+    assert L.dptq_select_layers(0, FAKE, FAKE, 0.0, 0.0, ctypes.cast(out, ctypes.c_void_p)) == INVALID
+
+
 def test_prepare_weights_validation(L):
     f = L.dptq_prepare_weights
     assert f(FAKE, 16, 256, 100, FAKE, FAKE, NULL) == INVALID
