@@ -239,6 +239,88 @@ def time_decode(torch, dptq, args):
     return out
 
 
+def time_calibration(torch, dptq):
+    """Residual-dynamics calibration (Eq. 8-11) of one 4096-wide layer over a
+    2048-token batch: per-token JR and SNR plus the layer means, graph-replayed
+    over 12 input copies; GB/s counts reading x and dx once and writing the
+    statistics."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    T, K, h = 2048, 4096, 4096
+    x, dx = workloads.residual_stream(np.random.default_rng(11), 2, T, K)[0]
+    R = 12
+    xs = [torch.from_numpy(x).to(dev) for _ in range(R)]
+    dxs = [torch.from_numpy(dx).to(dev) for _ in range(R)]
+    jr = torch.empty(T, dtype=torch.float32, device=dev)
+    snr = torch.empty(T, dtype=torch.float32, device=dev)
+    means = torch.empty(2, dtype=torch.float64, device=dev)
+    out = {}
+    for bits in (4, 8):
+        us = _graph_time(torch, [
+            (lambda i: (lambda: dptq.residual_dynamics(xs[i % R], dxs[i % R], h, bits,
+                                                       jr=jr, snr=snr, means=means)))(i)
+            for i in range(24)])
+        nbytes = 2 * 2 * T * K + 8 * T + 16
+        out[f"residual_dynamics_a{bits}"] = {"us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
+    return out
+
+
+def time_stack(torch, dptq, name, Ms, reps=3):
+    """End-to-end time of every linear of a whole layer stack (rotate+quantize
+    and GEMM per linear, layer bits from the policy), captured as one HIP graph
+    per policy and replayed.  Each layer has its own weights (random packed
+    code bytes drawn on the device: the time does not depend on their values);
+    each linear's input is the seeded stack input of a mid-stack layer.
+    Returns ms per stack for all-4-bit, the paper's default set, a seeded
+    4-layer mask and all-8-bit activations, and the mixed/all-4-bit ratios."""
+    import workloads
+    dev = torch.device("cuda:0")
+    cfg = workloads.CONFIGS[name]
+    L, lins = cfg["L"], cfg["linears"]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg["seed"])
+    W = [[(torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen),
+           torch.rand(N, device=dev, generator=gen) * 1e-3 + 1e-4)
+          for _, K, N, _ in lins] for _ in range(L)]
+    wbytes = sum(N * K // 2 + 4 * N for _, K, N, _ in lins) * L
+    policies = {"all_a4": [4] * L, "default": dptq.layer_policy(L),
+                "seeded_mask": dptq.layer_policy(L, workloads.layer_mask(L, 4, cfg["mask_seed"])),
+                "all_a8": [8] * L}
+    out = {"weights_GB": round(wbytes / 1e9, 2)}
+    for M in Ms:
+        X = [torch.from_numpy(workloads.stack_layer_input(name, L // 2, n, M=M)).to(dev)
+             for n, *_ in lins]
+        Kmax = max(K for _, K, _, _ in lins)
+        Nmax = max(N for _, _, N, _ in lins)
+        cbuf = torch.empty(M * Kmax, dtype=torch.uint8, device=dev)
+        sbuf = torch.empty(M, dtype=torch.float32, device=dev)
+        ybuf = torch.empty(M * Nmax, dtype=torch.float16, device=dev)
+        res = {}
+        for pname, bits in policies.items():
+            def run(bits=bits):
+                for l in range(L):
+                    b = bits[l]
+                    for i, (_, K, N, h) in enumerate(lins):
+                        dt = torch.uint8 if b == 4 else torch.int8
+                        codes = cbuf[: M * K * b // 8].view(dt).view(M, K * b // 8)
+                        dptq.rotate_quant(X[i], h, b, codes, sbuf)
+                        dptq.qlinear(codes, sbuf, b, W[l][i][0], W[l][i][1],
+                                     ybuf[: M * N].view(M, N))
+            res[pname] = _graph_time(torch, [run], reps=reps) / 1e3
+        ops = 2.0 * M * sum(K * N for _, K, N, _ in lins) * L
+        ent = {f"{p}_ms": round(v, 3) for p, v in res.items()}
+        ent["default_over_all_a4"] = round(res["default"] / res["all_a4"], 4)
+        ent["seeded_mask_over_all_a4"] = round(res["seeded_mask"] / res["all_a4"], 4)
+        ent["all_a4_TOPS"] = round(ops / (res["all_a4"] * 1e-3) / 1e12, 1)
+        ent["all_a4_weight_GB/s"] = round(wbytes / (res["all_a4"] * 1e-3) / 1e9, 1)
+        out[f"M{M}"] = ent
+        del X, cbuf, ybuf
+    del W
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(cfg, rows, seed=123):
     """Time the CPU oracle on a bounded sample: `rows` token rows of the same
     layer, both precisions (rotation + quantization + exact GEMM + epilogue)."""
@@ -316,6 +398,9 @@ def main():
     }
     if args.extended:
         rec["decode"] = time_decode(torch, dptq, args)
+        rec["calibration"] = time_calibration(torch, dptq)
+        rec["stacks"] = {"llama2_7b_32_layers": time_stack(torch, dptq, "llama2_7b_stack", (2048, 8)),
+                         "llama2_70b_80_layers": time_stack(torch, dptq, "llama2_70b_layer", (4096, 8))}
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(cfg, args.cpu_rows)
     print(json.dumps(rec), flush=True)

@@ -18,7 +18,8 @@ shapes and value structure:
 import numpy as np
 
 __all__ = ["CONFIGS", "gauss_massive", "gauss_outliers", "student_t",
-           "residual_phase", "residual_stream", "weights", "layer_mask", "activations_for"]
+           "residual_phase", "residual_stream", "weights", "layer_mask", "activations_for",
+           "stack_layer_input", "stack_weights"]
 
 # name -> description.  Linear tuples are (name, K, N, had_size).
 CONFIGS = {
@@ -33,7 +34,7 @@ CONFIGS = {
                                      ("o", 4096, 4096, 4096),
                                      ("gate_up", 4096, 22016, 4096),
                                      ("down", 11008, 4096, 256)]),
-    "llama2_70b_layer": dict(L=80, Ms=(4096, 8), seed=5, mask_seed=5,
+    "llama2_70b_layer": dict(L=80, M=4096, Ms=(4096, 8), seed=5, mask_seed=5,
                              linears=[("qkv", 8192, 10240, 8192),
                                       ("o", 8192, 8192, 8192),
                                       ("gate_up", 8192, 57344, 8192),
@@ -170,3 +171,36 @@ def random_weight_bytes(rng, N, K):
 def random_scales(rng, n, lo=1e-4, hi=1e-1):
     """Seeded positive fp32 scales."""
     return rng.uniform(lo, hi, n).astype(np.float32)
+
+
+def stack_layer_input(name, layer, linear, M=None):
+    """Input of one linear of one layer of a stack config, fp16 [M, K].
+
+    llama2_7b_stack: the qkv and gate_up inputs follow the residual model
+    (massive channels switched on inside the stack's seeded phase window),
+    o inputs are N(0,1) and down inputs Student-t(3).  llama2_70b_layer: the
+    qkv, o and gate_up inputs are N(0,1) with outlier channels as in the
+    7B QKV config, down inputs Student-t(3).  Every (layer, linear) pair has
+    its own seed."""
+    cfg = CONFIGS[name]
+    lin = {n: (K, N, h) for n, K, N, h in cfg["linears"]}
+    K = lin[linear][0]
+    M = cfg["M"] if M is None else M
+    order = [n for n, *_ in cfg["linears"]].index(linear)
+    rng = np.random.default_rng([cfg["seed"], layer, order])
+    if linear == "down":
+        return student_t(rng, M, K)
+    if name == "llama2_7b_stack":
+        if linear == "o":
+            return _to_f16(rng.standard_normal((M, K), dtype=np.float32))
+        plan = residual_phase_plan(np.random.default_rng(cfg["seed"]), K, cfg["L"])
+        return residual_phase(rng, M, K, layer, *plan)
+    return gauss_outliers(rng, M, K)
+
+
+def stack_weights(name, layer, linear):
+    """fp32 weights [N, K] of one linear of one layer of a stack config."""
+    cfg = CONFIGS[name]
+    names = [n for n, *_ in cfg["linears"]]
+    _, K, N, _ = cfg["linears"][names.index(linear)]
+    return weights(np.random.default_rng([cfg["seed"], layer, names.index(linear), 1]), N, K)
