@@ -21,6 +21,8 @@ Modules
   policy    phase-aware activation bit policy (Eq. 21, Algorithm 1 step 2).
   residual  Jump Ratio, Historical Feature SNR and the sensitive-layer rule
             (Section 3.1 Eq. 8-11, Section 3.3 Eq. 20).
+  kv        group-wise 4-bit KV-cache quantizer and its reconstruction
+            (Section 4.2, Eq. 1-2).
 """
 
 from .hadamard import (sylvester, paley28, hadamard, split_had_size,
@@ -31,6 +33,7 @@ from .gemm import qlinear_acc_ref, qlinear_acc_entries, epilogue_ref, qlinear_re
 from .policy import layer_policy_ref
 from .residual import (jump_ratio_tokens_ref, inverse_rotate_f64, reconstructed_history_ref,
                        hist_snr_tokens_ref, residual_dynamics_ref, select_sensitive_layers_ref)
+from .kv import kv_quant_ref, kv_dequant_ref, pack_u4, unpack_u4
 
 __all__ = [
     "sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows",
@@ -40,4 +43,5 @@ __all__ = [
     "layer_policy_ref",
     "jump_ratio_tokens_ref", "inverse_rotate_f64", "reconstructed_history_ref",
     "hist_snr_tokens_ref", "residual_dynamics_ref", "select_sensitive_layers_ref",
+    "kv_quant_ref", "kv_dequant_ref", "pack_u4", "unpack_u4",
 ]
