@@ -266,6 +266,33 @@ def time_calibration(torch, dptq):
     return out
 
 
+def time_kv(torch, dptq):
+    """Group-wise KV4 codec on one layer's keys of a 32-sequence x 2048-token
+    prefill for LLaMA-3-8B (8 KV heads x 128 = 1024 per token, group 128):
+    quantize and reconstruct, graph-replayed over 4 distinct caches (> 256 MiB
+    each way).  Algorithmic bytes: 2 B in, 0.5 B of codes and 8 B of (s, m)
+    per 128-element group out, and the reverse for the reconstruction."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    T, D, g = 32 * 2048, 1024, 128
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(8)
+    R = 4
+    xs = [torch.randn((T, D), device=dev, generator=gen).half() for _ in range(R)]
+    outs = [dptq.kv_quant(x, g) for x in xs]
+    rec = [torch.empty((T, D), dtype=torch.float16, device=dev) for _ in range(R)]
+    nbytes = 2 * T * D + T * D // 2 + 8 * T * (D // g)
+    q_us = _graph_time(torch, [
+        (lambda i: (lambda: dptq.kv_quant(xs[i % R], g, *outs[i % R])))(i) for i in range(8)])
+    d_us = _graph_time(torch, [
+        (lambda i: (lambda: dptq.kv_dequant(*outs[i % R], g, out=rec[i % R])))(i) for i in range(8)])
+    del xs, outs, rec
+    torch.cuda.empty_cache()
+    return {"tokens": T, "row": D, "group": g,
+            "quant_us": round(q_us, 2), "quant_GB/s": round(nbytes / q_us / 1e3, 1),
+            "dequant_us": round(d_us, 2), "dequant_GB/s": round(nbytes / d_us / 1e3, 1)}
+
+
 def time_stack(torch, dptq, name, Ms, reps=3):
     """End-to-end time of every linear of a whole layer stack (rotate+quantize
     and GEMM per linear, layer bits from the policy), captured as one HIP graph
@@ -399,6 +426,7 @@ def main():
     if args.extended:
         rec["decode"] = time_decode(torch, dptq, args)
         rec["calibration"] = time_calibration(torch, dptq)
+        rec["kv4"] = time_kv(torch, dptq)
         rec["stacks"] = {"llama2_7b_32_layers": time_stack(torch, dptq, "llama2_7b_stack", (2048, 8)),
                          "llama2_70b_80_layers": time_stack(torch, dptq, "llama2_70b_layer", (4096, 8))}
     if not args.no_cpu_baseline:

@@ -153,8 +153,8 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
  * the inverse rotation.  The error energy is taken in the rotated space and
  * divided by h, which equals ||Q_b(u) - u||^2 for the unnormalized H_h.
  * Norms and error energy accumulate in fp32 (any order), the final
- * arithmetic is fp64; results agree with an fp64 evaluation to about 1e-5
- * relative (JR) and 1e-4 dB (SNR).
+ * arithmetic is fp64; results agree with an fp64 evaluation within 2e-5
+ * relative (JR) and 1e-3 dB (SNR).
  *
  *   x, dx       device, fp16 [T, K], row-major, 16-byte aligned
  *   T, K, had_size   as for dptq_rotate_quant
@@ -178,6 +178,42 @@ int dptq_residual_dynamics(const void* x, const void* dx, int64_t T, int64_t K, 
  */
 int dptq_select_layers(int32_t num_layers, const double* jr, const double* snr, double tau_jr,
                        double tau_snr, int32_t* bits_out);
+
+/*
+ * dptq_kv_quant - group-wise 4-bit KV-cache quantization (Section 4.2: KV cache
+ * at 4 bits with groups of 128; Eq. 1 range step, Eq. 2 rounding).
+ *
+ * Each row of kv is split into groups of `group` consecutive elements (with
+ * head_dim 128 and group 128, one head of one token).  Per group, with m the
+ * minimum and M the maximum:
+ *
+ *   s = fl32(fl32(M - m) / 15)                     (2^4 - 1 intervals, Eq. 1)
+ *   code = min(15, RNE(fl32(fl32(x - m) / s)))     (Eq. 2 on the offset; 0 if s = 0)
+ *
+ * IEEE fp32 arithmetic, round half to even.
+ *
+ *   kv      device, fp16 [T, D], row-major, 16-byte aligned (K or V rows of T tokens)
+ *   T       tokens, >= 0
+ *   D       row length; a multiple of group, <= 2^31, T * D < 2^40
+ *   group   power of two in [16, 512]
+ *   codes   device, uint8 [T, D/2] output, 4-byte aligned: byte j of a row holds
+ *           code[2j] in its low nibble and code[2j+1] in its high nibble
+ *   scales  device, float [T, D/group] output (s per group), 4-byte aligned
+ *   mins    device, float [T, D/group] output (m per group), 4-byte aligned
+ *
+ * To append tokens to a cache, pass pointers offset to the first new row.
+ * Non-finite inputs give unspecified codes.  T = 0 enqueues nothing.
+ */
+int dptq_kv_quant(const void* kv, int64_t T, int64_t D, int32_t group, uint8_t* codes,
+                  float* scales, float* mins, void* stream);
+
+/*
+ * dptq_kv_dequant - reconstruct the fp16 cache from dptq_kv_quant's output:
+ * kv_out = fl16(fl32(fl32(code * s) + m)), two fp32 roundings then one fp16.
+ * Arguments as for dptq_kv_quant; kv_out is device fp16 [T, D], 16-byte aligned.
+ */
+int dptq_kv_dequant(const uint8_t* codes, const float* scales, const float* mins, int64_t T,
+                    int64_t D, int32_t group, void* kv_out, void* stream);
 
 /*
  * dptq_layer_policy - phase-aware activation precision (host only).

@@ -15,7 +15,8 @@ import ctypes
 import os
 
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
-           "layer_policy", "prepare_weights", "residual_dynamics", "select_layers", "version",
+           "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
+           "kv_quant", "kv_dequant", "version",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
@@ -27,6 +28,7 @@ _lib = None
 EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_qlinear", "dptq_qlinear_acc", "dptq_qlinear_kernel",
                       "dptq_residual_dynamics", "dptq_select_layers",
+                      "dptq_kv_quant", "dptq_kv_dequant",
                       "dptq_layer_policy", "dptq_prepare_weights")
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
@@ -71,6 +73,10 @@ def lib():
         L.dptq_residual_dynamics.restype = ctypes.c_int
         L.dptq_select_layers.argtypes = [i32, vp, vp, ctypes.c_double, ctypes.c_double, vp]
         L.dptq_select_layers.restype = ctypes.c_int
+        L.dptq_kv_quant.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
+        L.dptq_kv_quant.restype = ctypes.c_int
+        L.dptq_kv_dequant.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp]
+        L.dptq_kv_dequant.restype = ctypes.c_int
         L.dptq_layer_policy.argtypes = [i32, vp, vp]
         L.dptq_layer_policy.restype = ctypes.c_int
         L.dptq_prepare_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp]
@@ -242,6 +248,50 @@ def select_layers(jr_layers, snr_layers, tau_jr, tau_snr):
                                     float(tau_jr), float(tau_snr), ctypes.cast(out, ctypes.c_void_p)),
            "dptq_select_layers")
     return list(out)
+
+
+def kv_quant(kv, group=128, codes=None, scales=None, mins=None):
+    """Group-wise 4-bit quantization of fp16 KV rows kv [T, D] ->
+    (codes uint8 [T, D/2], scales float32 [T, D/group], mins float32 [T, D/group])."""
+    torch = _torch()
+    _require(kv, "kv", torch.float16)
+    if kv.dim() != 2:
+        raise ValueError("kv must be 2-D [T, D]")
+    T, D = kv.shape
+    if group <= 0 or D % group:
+        raise ValueError("D must be a multiple of group")
+    G = D // group
+    if codes is None:
+        codes = torch.empty((T, D // 2), dtype=torch.uint8, device=kv.device)
+    if scales is None:
+        scales = torch.empty((T, G), dtype=torch.float32, device=kv.device)
+    if mins is None:
+        mins = torch.empty((T, G), dtype=torch.float32, device=kv.device)
+    _require(codes, "codes", torch.uint8, (T, D // 2))
+    _require(scales, "scales", torch.float32, (T, G))
+    _require(mins, "mins", torch.float32, (T, G))
+    _check(lib().dptq_kv_quant(_ptr(kv), T, D, int(group), _ptr(codes), _ptr(scales), _ptr(mins),
+                               _stream(kv)), "dptq_kv_quant")
+    return codes, scales, mins
+
+
+def kv_dequant(codes, scales, mins, group=128, out=None):
+    """Reconstruct fp16 [T, D] from kv_quant's output."""
+    torch = _torch()
+    _require(codes, "codes", torch.uint8)
+    if codes.dim() != 2:
+        raise ValueError("codes must be 2-D [T, D/2]")
+    T, D = codes.shape[0], 2 * codes.shape[1]
+    if group <= 0 or D % group:
+        raise ValueError("D must be a multiple of group")
+    _require(scales, "scales", torch.float32, (T, D // group))
+    _require(mins, "mins", torch.float32, (T, D // group))
+    if out is None:
+        out = torch.empty((T, D), dtype=torch.float16, device=codes.device)
+    _require(out, "out", torch.float16, (T, D))
+    _check(lib().dptq_kv_dequant(_ptr(codes), _ptr(scales), _ptr(mins), T, D, int(group),
+                                 _ptr(out), _stream(codes)), "dptq_kv_dequant")
+    return out
 
 
 def layer_policy(num_layers, mask=None):

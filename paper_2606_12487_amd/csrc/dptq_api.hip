@@ -52,6 +52,17 @@ int check_gemm_shape(int64_t M, int64_t K, int32_t bits, int64_t N) {
 
 int from_hip(hipError_t e) { return e == hipSuccess ? DPTQ_OK : DPTQ_ERR_HIP; }
 
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+// KV-cache shapes: group a power of two in [16, 512] dividing D; T * D < 2^40.
+int check_kv_shape(int64_t T, int64_t D, int32_t group) {
+  if (T < 0 || D < 1) return DPTQ_ERR_INVALID_ARG;
+  if (group < 16 || group > 512 || (group & (group - 1)) != 0) return DPTQ_ERR_INVALID_ARG;
+  if (D % group != 0) return DPTQ_ERR_INVALID_ARG;
+  if (D > (int64_t{1} << 31) || T > (int64_t{1} << 40) / D) return DPTQ_ERR_UNSUPPORTED;
+  return DPTQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -130,6 +141,30 @@ int dptq_select_layers(int32_t num_layers, const double* jr, const double* snr, 
   for (int32_t l = 0; l < num_layers; ++l)
     bits_out[l] = (jr[l] > tau_jr && snr[l] < tau_snr) ? 8 : 4;
   return DPTQ_OK;
+}
+
+int dptq_kv_quant(const void* kv, int64_t T, int64_t D, int32_t group, uint8_t* codes,
+                  float* scales, float* mins, void* stream) {
+  const int st = check_kv_shape(T, D, group);
+  if (st != DPTQ_OK) return st;
+  if (T == 0) return DPTQ_OK;
+  if (!kv || !codes || !scales || !mins) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(kv) || !aligned4(codes) || !aligned4(scales) || !aligned4(mins))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_kv_quant(kv, T, D, group, codes, scales, mins,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+int dptq_kv_dequant(const uint8_t* codes, const float* scales, const float* mins, int64_t T,
+                    int64_t D, int32_t group, void* kv_out, void* stream) {
+  const int st = check_kv_shape(T, D, group);
+  if (st != DPTQ_OK) return st;
+  if (T == 0) return DPTQ_OK;
+  if (!kv_out || !codes || !scales || !mins) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(kv_out) || !aligned4(codes) || !aligned4(scales) || !aligned4(mins))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_kv_dequant(codes, scales, mins, T, D, group, kv_out,
+                                          static_cast<hipStream_t>(stream)));
 }
 
 int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int64_t K,

@@ -30,6 +30,13 @@ hipError_t launch_residual_stats(const void* x, const void* dx, int64_t T, int K
                                  int bits, float eps, float* jr, float* snr, double* means,
                                  hipStream_t stream);
 
+// Group-wise 4-bit KV-cache codec over fp16 [T, D]; group in {16, ..., 512}
+// (a power of two dividing D).
+hipError_t launch_kv_quant(const void* kv, int64_t T, int64_t D, int group, uint8_t* codes,
+                           float* scales, float* mins, hipStream_t stream);
+hipError_t launch_kv_dequant(const uint8_t* codes, const float* scales, const float* mins,
+                             int64_t T, int64_t D, int group, void* out, hipStream_t stream);
+
 // GEMM kernels (values of dptq_gemm_kernel).
 constexpr int kGemmAuto = 0, kGemmDecode = 1, kGemmTile = 2, kGemmWide = 3;
 

@@ -182,6 +182,34 @@ def test_select_layers_matches_oracle(L):
     assert L.dptq_select_layers(0, FAKE, FAKE, 0.0, 0.0, ctypes.cast(out, ctypes.c_void_p)) == INVALID
 
 
+def kvq(L, kv=FAKE, T=4, D=256, group=128, codes=FAKE, scales=FAKE, mins=FAKE):
+    return L.dptq_kv_quant(kv, T, D, group, codes, scales, mins, NULL)
+
+
+def kvd(L, codes=FAKE, scales=FAKE, mins=FAKE, T=4, D=256, group=128, out=FAKE):
+    return L.dptq_kv_dequant(codes, scales, mins, T, D, group, out, NULL)
+
+
+def test_kv_codec_validation(L):
+    for f in (kvq, kvd):
+        assert f(L, group=96) == INVALID                  # not a power of two
+        assert f(L, group=8) == INVALID
+        assert f(L, group=1024) == INVALID
+        assert f(L, D=320) == INVALID                     # not a multiple of the group
+        assert f(L, T=-1) == INVALID
+        assert f(L, D=0) == INVALID
+        assert f(L, T=1 << 30, D=4096) == UNSUPPORTED     # T * D >= 2^40
+        assert f(L, scales=NULL) == INVALID
+        assert f(L, mins=NULL) == INVALID
+        assert f(L, codes=ctypes.c_void_p(0x10002)) == INVALID
+        assert f(L, scales=ctypes.c_void_p(0x10002)) == INVALID
+        assert f(L, T=0, codes=NULL, scales=NULL, mins=NULL) == OK
+    assert kvq(L, kv=NULL) == INVALID
+    assert kvq(L, kv=MISALIGNED) == INVALID
+    assert kvd(L, out=NULL) == INVALID
+    assert kvd(L, out=MISALIGNED) == INVALID
+
+
 def test_prepare_weights_validation(L):
     f = L.dptq_prepare_weights
     assert f(FAKE, 16, 256, 100, FAKE, FAKE, NULL) == INVALID
