@@ -243,6 +243,58 @@ int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out
 int dptq_prepare_weights(const float* w, int64_t N, int64_t K, int32_t had_size,
                          uint8_t* w_packed, float* w_scales, void* stream);
 
+/*
+ * FP6 operand path of the 4-bit x 4-bit GEMM.  The same integer product as
+ * dptq_qlinear at bits 4 (Section 2, Y = X W^T; Section 4.2 scales) computed
+ * on the FP6 matrix cores: every 4-bit code c in [-8, 7] is stored as the
+ * e2m3 value c / 2 (exact) and multiplied with a block scale of 2 per
+ * operand, so each product is the exact integer a * w and the fp32
+ * accumulation is exact (|partial sums| <= 64 K <= 2^22).  Results equal
+ * dptq_qlinear's bit for bit.
+ *
+ * FP6 block layout of a [rows, K] code matrix (K % 128 == 0): rows padded to
+ * Rp = 32 * ceil(rows / 32) with zero codes; blocks of 32 rows x 128 k, block
+ * (rb, kb) at byte offset (kb * Rp/32 + rb) * 3072.  A block is two halves of
+ * 1536 bytes, s = 0, 1.  In half s, lane l = 0..63 owns row 32 rb + (l & 31)
+ * and codes k = 128 kb + 64 (l >> 5) + 32 s + j, j = 0..31, as a 192-bit
+ * little-endian value whose bits 6 j .. 6 j + 5 hold the e2m3 field of code
+ * j; its bytes 8 c .. 8 c + 7 (c = 0, 1, 2) sit at byte 1536 s + 512 c + 8 l.
+ */
+
+/* Bytes of the FP6 block layout of a [rows, K] code matrix; -1 when rows < 0
+   or K is not a multiple of 128 in [128, DPTQ_MAX_K]. */
+int64_t dptq_fp6_bytes(int64_t rows, int64_t K);
+
+/*
+ * dptq_pack_fp6 - canonical packed 4-bit codes -> FP6 block layout.  Serves
+ * weights (once, offline) and activation codes (per call, after
+ * dptq_rotate_quant at bits 4).
+ *
+ *   codes  device, uint8 [rows, K/2] in the dptq_rotate_quant 4-bit layout
+ *   rows   >= 0 (0 enqueues nothing); K multiple of 128, <= DPTQ_MAX_K
+ *   out    device, dptq_fp6_bytes(rows, K) bytes, 16-byte aligned; padding
+ *          rows are written as zero codes
+ */
+int dptq_pack_fp6(const uint8_t* codes, int64_t rows, int64_t K, uint8_t* out, void* stream);
+
+/*
+ * dptq_qlinear_fp6 - dptq_qlinear at bits 4 on FP6 operands: y (fp16 [M, N])
+ * from the dequant epilogue when y != NULL (a_scales, w_scales required), or
+ * the raw int32 accumulators when acc != NULL (device int32 [M, N]; scales
+ * ignored).  Exactly one of y and acc.
+ *
+ *   a_fp6    device, FP6 block layout of the [M, K] activation codes
+ *   w_fp6    device, FP6 block layout of the [N, K] weight codes
+ *   a_scales device, float [M]; w_scales device, float [N] (4-byte aligned)
+ *   M >= 0, K multiple of 128 in [128, DPTQ_MAX_K], N multiple of 16
+ *
+ * Any M runs (the kernel tiles 256 tokens x 192 channels; it pays off for
+ * prefill shapes, M in the hundreds and above).
+ */
+int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int64_t K,
+                     const uint8_t* w_fp6, const float* w_scales, int64_t N, void* y,
+                     int32_t* acc, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -16,7 +16,8 @@ import os
 
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
            "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
-           "kv_quant", "kv_dequant", "version",
+           "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "qlinear_fp6",
+           "qlinear_fp6_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
@@ -29,7 +30,8 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_qlinear", "dptq_qlinear_acc", "dptq_qlinear_kernel",
                       "dptq_residual_dynamics", "dptq_select_layers",
                       "dptq_kv_quant", "dptq_kv_dequant",
-                      "dptq_layer_policy", "dptq_prepare_weights")
+                      "dptq_layer_policy", "dptq_prepare_weights",
+                      "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_qlinear_fp6")
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
 GEMM_AUTO, GEMM_DECODE, GEMM_TILE_256X128, GEMM_TILE_192X256 = 0, 1, 2, 3
@@ -81,6 +83,12 @@ def lib():
         L.dptq_layer_policy.restype = ctypes.c_int
         L.dptq_prepare_weights.argtypes = [vp, i64, i64, i32, vp, vp, vp]
         L.dptq_prepare_weights.restype = ctypes.c_int
+        L.dptq_fp6_bytes.argtypes = [i64, i64]
+        L.dptq_fp6_bytes.restype = ctypes.c_int64
+        L.dptq_pack_fp6.argtypes = [vp, i64, i64, vp, vp]
+        L.dptq_pack_fp6.restype = ctypes.c_int
+        L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
+        L.dptq_qlinear_fp6.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -327,3 +335,60 @@ def prepare_weights(w, had_size, w_packed=None, w_scales=None):
     _check(lib().dptq_prepare_weights(_ptr(w), N, K, int(had_size), _ptr(w_packed),
                                       _ptr(w_scales), _stream(w)), "dptq_prepare_weights")
     return w_packed, w_scales
+
+
+def fp6_bytes(rows, K):
+    """Bytes of the FP6 block layout of a [rows, K] matrix of 4-bit codes."""
+    n = lib().dptq_fp6_bytes(int(rows), int(K))
+    if n < 0:
+        raise ValueError(f"no FP6 layout for rows={rows}, K={K} (K must be a multiple of 128)")
+    return n
+
+
+def pack_fp6(codes, out=None):
+    """Packed 4-bit codes [R, K/2] (activations or weights) -> FP6 block layout
+    (uint8 [fp6_bytes(R, K)]), the operand format of qlinear_fp6."""
+    torch = _torch()
+    _require(codes, "codes", torch.uint8)
+    if codes.dim() != 2:
+        raise ValueError("codes must be 2-D [R, K/2]")
+    R, K = codes.shape[0], codes.shape[1] * 2
+    n = fp6_bytes(R, K)
+    if out is None:
+        out = torch.empty((n,), dtype=torch.uint8, device=codes.device)
+    _require(out, "out", torch.uint8, (n,))
+    _check(lib().dptq_pack_fp6(_ptr(codes), R, K, _ptr(out), _stream(codes)), "dptq_pack_fp6")
+    return out
+
+
+def _fp6_args(a6, w6, M, K, N):
+    torch = _torch()
+    _require(a6, "a_fp6", torch.uint8, (fp6_bytes(M, K),))
+    _require(w6, "w_fp6", torch.uint8, (fp6_bytes(N, K),))
+
+
+def qlinear_fp6(a6, a_scales, w6, w_scales, M, K, N, y=None):
+    """y [M, N] fp16 = dequant(a . w^T) for 4-bit codes in the FP6 block layout
+    (the same bits as qlinear at 4 bits)."""
+    torch = _torch()
+    _fp6_args(a6, w6, M, K, N)
+    _require(a_scales, "a_scales", torch.float32, (M,))
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=a6.device)
+    _require(y, "y", torch.float16, (M, N))
+    _check(lib().dptq_qlinear_fp6(_ptr(a6), _ptr(a_scales), M, K, _ptr(w6), _ptr(w_scales), N,
+                                  _ptr(y), None, _stream(a6)), "dptq_qlinear_fp6")
+    return y
+
+
+def qlinear_fp6_acc(a6, w6, M, K, N, acc=None):
+    """Raw int32 accumulators [M, N] of the FP6 GEMM (exact)."""
+    torch = _torch()
+    _fp6_args(a6, w6, M, K, N)
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=a6.device)
+    _require(acc, "acc", torch.int32, (M, N))
+    _check(lib().dptq_qlinear_fp6(_ptr(a6), None, M, K, _ptr(w6), None, N, None, _ptr(acc),
+                                  _stream(a6)), "dptq_qlinear_fp6")
+    return acc

@@ -19,11 +19,11 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libdptq.so")
 
-SOURCES = ["dptq_api.hip", "rotate_quant.hip", "qgemm.hip", "kv_quant.hip"]
+SOURCES = ["dptq_api.hip", "rotate_quant.hip", "qgemm.hip", "qgemm_fp6.hip", "kv_quant.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
     "-ffp-contract=off", "-fno-fast-math",
     # packed fp32 ALU forms are kept out of the generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -189,6 +189,41 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
                                        nullptr, acc, kernel, static_cast<hipStream_t>(stream)));
 }
 
+int64_t dptq_fp6_bytes(int64_t rows, int64_t K) {
+  if (rows < 0 || K < 128 || K % 128 != 0 || K > DPTQ_MAX_K || rows > 0x7FFFFFFF) return -1;
+  return dptq::fp6_bytes(rows, K);
+}
+
+int dptq_pack_fp6(const uint8_t* codes, int64_t rows, int64_t K, uint8_t* out, void* stream) {
+  if (rows < 0 || K < 1) return DPTQ_ERR_INVALID_ARG;
+  if (K % 128 != 0 || K > DPTQ_MAX_K || rows > 0x7FFFFFFF) return DPTQ_ERR_UNSUPPORTED;
+  if (rows == 0) return DPTQ_OK;
+  if (!codes || !out) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(out)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_pack_fp6(codes, rows, (int)K, out, static_cast<hipStream_t>(stream)));
+}
+
+int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int64_t K,
+                     const uint8_t* w_fp6, const float* w_scales, int64_t N, void* y,
+                     int32_t* acc, void* stream) {
+  int st = check_gemm_shape(M, K, 4, N);
+  if (st != DPTQ_OK) return st;
+  if ((y == nullptr) == (acc == nullptr)) return DPTQ_ERR_INVALID_ARG;
+  if (((M + 255) / 256) * ((N + 191) / 192) > 0x7FFFFFFF) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!a_fp6 || !w_fp6) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(a_fp6) || !aligned16(w_fp6)) return DPTQ_ERR_INVALID_ARG;
+  if (y) {
+    if (!a_scales || !w_scales) return DPTQ_ERR_INVALID_ARG;
+    if (!aligned4(a_scales) || !aligned4(w_scales) || !aligned16(y)) return DPTQ_ERR_INVALID_ARG;
+  } else if (!aligned16(acc)) {
+    return DPTQ_ERR_INVALID_ARG;
+  }
+  return from_hip(dptq::launch_qlinear_fp6(a_fp6, y ? a_scales : nullptr, M, (int)K, w_fp6,
+                                           y ? w_scales : nullptr, N, y, y ? nullptr : acc,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {
   if (num_layers < 1 || !bits_out) return DPTQ_ERR_INVALID_ARG;
   for (int32_t l = 0; l < num_layers; ++l) {

@@ -49,4 +49,19 @@ hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
                           const float* w_scales, int64_t N, void* y,
                           int32_t* out_acc, int kernel, hipStream_t stream);
 
+// Compute units of the current device (cached per device).
+int device_cus();
+
+// FP6 block layout of 4-bit codes (e2m3(c / 2), 32-row x 128-k blocks of
+// 3072 bytes; see qgemm_fp6.hip): bytes for a [rows, K] code matrix.
+int64_t fp6_bytes(int64_t rows, int64_t K);
+// Canonical packed 4-bit codes [R, K/2] -> FP6 block layout (K % 128 == 0).
+hipError_t launch_pack_fp6(const uint8_t* codes, int64_t R, int K, uint8_t* out,
+                           hipStream_t stream);
+// W4A4 GEMM on the FP6 matrix cores; operands in the FP6 block layout.
+// out_acc != nullptr selects the raw int32 accumulator output.
+hipError_t launch_qlinear_fp6(const uint8_t* a6, const float* a_scales, int64_t M, int K,
+                              const uint8_t* w6, const float* w_scales, int64_t N, void* y,
+                              int32_t* out_acc, hipStream_t stream);
+
 }  // namespace dptq

@@ -919,20 +919,6 @@ void launch_wide(const uint8_t* a, const float* as, int64_t M, int K, const uint
                      stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
 }
 
-// Compute units of the current device (cached per device).
-int device_cus() {
-  static int cache[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cache[dev] == 0) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
-      v = 256;
-    cache[dev] = v;
-  }
-  return cache[dev];
-}
-
 // Relative time of a launch: rounds of one tile per compute unit, times the
 // tile's area over the measured throughput of the tile shape.
 double launch_cost(int64_t M, int64_t N, int bm, int bn, double speed, int cus) {
@@ -987,6 +973,20 @@ hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
 }
 
 }  // namespace
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+      v = 256;
+    cache[dev] = v;
+  }
+  return cache[dev];
+}
 
 bool gemm_kernel_fits(int kernel, int64_t M, int64_t N, int K, int bits) {
   switch (kernel) {

@@ -26,7 +26,7 @@ NULL = ctypes.c_void_p(0)
 def _declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dptq_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(dptq_[a-z0-9_]+)\s*\(", text)))
 
 
 @pytest.fixture(scope="module")

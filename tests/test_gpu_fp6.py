@@ -1,0 +1,227 @@
+"""GPU parity of the FP6 operand path: the 4-bit x 4-bit GEMM computed on the
+FP6 (e2m3) matrix cores, through the C ABI, against the CPU oracle.
+
+Bar: int32 accumulators and fp16 outputs bit for bit against the oracle's
+exact integer GEMM and pinned epilogue (the FP6 path computes the same exact
+integer product, so nothing looser applies), and the FP6 block layout byte for
+byte against a reference encoder written here from the e2m3 definition (sign,
+two exponent bits with bias 1, three mantissa bits; subnormals m / 8).  Inputs
+are seeded random code bytes (every nibble value, -8 included) so no oracle
+input comes from the HIP path.  Full-size shapes are checked whole against the
+int8 path (itself parity-tested against the oracle) and on sampled entries
+against the oracle directly.
+"""
+
+import numpy as np
+import pytest
+
+import workloads
+from oracle import (rotate_quant_ref, prepare_weights_ref, qlinear_acc_ref, epilogue_ref,
+                    unpack_int4)
+from oracle.gemm import qlinear_acc_entries
+
+torch = pytest.importorskip("torch")
+dptq = pytest.importorskip("paper_2606_12487_amd")
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    dptq.lib()
+    return torch.device("cuda:0")
+
+
+def _d(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def _h(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _e2m3_value(bits6):
+    s = -1.0 if bits6 & 0x20 else 1.0
+    e, m = (bits6 >> 3) & 3, bits6 & 7
+    return s * (m / 8.0 if e == 0 else 2.0 ** (e - 1) * (1.0 + m / 8.0))
+
+
+def _e2m3_table():
+    """Encoding of c / 2 for c = -8..7, found by decoding all 64 patterns."""
+    table = {}
+    for c in range(-8, 8):
+        hits = [b for b in range(64) if _e2m3_value(b) == c / 2.0 and not (c == 0 and b & 0x20)]
+        assert len(hits) == 1, (c, hits)
+        table[c] = hits[0]
+    return table
+
+
+def fp6_layout_ref(packed, K):
+    """Reference FP6 block layout of packed 4-bit codes [R, K/2] -> uint8 bytes."""
+    codes = unpack_int4(packed).astype(np.int64)             # [R, K], -8..7
+    R = codes.shape[0]
+    Rp = (R + 31) // 32 * 32
+    full = np.zeros((Rp, K), dtype=np.int64)
+    full[:R] = codes
+    tab = _e2m3_table()
+    lut = np.array([tab[c] for c in range(-8, 8)], dtype=np.uint64)
+    enc = lut[full + 8]                                      # [Rp, K] six-bit fields
+    nkb = K // 128
+    # k = 128 kb + 64 g + 32 s + j ; lane l = 32 g + r
+    e = enc.reshape(Rp // 32, 32, nkb, 2, 2, 32)             # rb, r, kb, g, s, j
+    e = e.transpose(0, 2, 4, 3, 1, 5).reshape(Rp // 32, nkb, 2, 64, 32)   # rb, kb, s, l, j
+    words = np.zeros(e.shape[:-1] + (3,), dtype=np.uint64)
+    for j in range(32):
+        pos = 6 * j
+        w, off = pos // 64, pos % 64
+        words[..., w] |= e[..., j] << np.uint64(off)
+        if off > 58:
+            words[..., w + 1] |= e[..., j] >> np.uint64(64 - off)
+    # plane c of half s holds bytes 8c..8c+7 (word c) of every lane, lane-major
+    planes = words.transpose(0, 1, 2, 4, 3).copy()           # rb, kb, s, c, l
+    blocks = planes.view(np.uint8).reshape(Rp // 32, nkb, 2 * 3 * 64 * 8)   # rb, kb, 3072
+    # blocks are stored k-block major: (kb, rb)
+    return blocks.transpose(1, 0, 2).reshape(-1)
+
+
+def test_e2m3_table_closed_form():
+    # c / 2 for the 16 codes: the table found by search is the one the layout
+    # states (sign bit 5, exponent bits 3-4, mantissa bits 0-2).
+    tab = _e2m3_table()
+    assert tab[0] == 0 and tab[1] == 0b000100 and tab[7] == 0b010110 and tab[-8] == 0b111000
+    for c in range(1, 8):
+        assert tab[-c] == tab[c] | 0x20
+
+
+@pytest.mark.parametrize("R,K", [(1, 128), (31, 256), (32, 128), (33, 640), (70, 384), (5, 4096)])
+def test_pack_fp6_layout(dev, R, K):
+    rng = np.random.default_rng(R * 7 + K)
+    packed = workloads.random_weight_bytes(rng, R, K)
+    got = _h(dptq.pack_fp6(_d(packed, dev)))
+    ref = fp6_layout_ref(packed, K)
+    assert got.shape == ref.shape == (dptq.fp6_bytes(R, K),)
+    bad = np.nonzero(got != ref)[0]
+    assert bad.size == 0, f"{bad.size} layout bytes differ, first at {bad[0]}"
+
+
+def _fp6_operands(dev, a_packed, w_packed):
+    return dptq.pack_fp6(_d(a_packed, dev)), dptq.pack_fp6(_d(w_packed, dev))
+
+
+GEMM_CASES = [
+    # (M, N, K): single tiles, ragged tiles in m and n, one and many stages,
+    # odd stage counts, several tiles per workgroup
+    (1, 16, 128), (17, 48, 256), (32, 192, 128), (255, 192, 384), (256, 192, 512),
+    (300, 208, 1024), (513, 400, 640), (600, 1008, 2048), (1024, 2304, 1152),
+    (257, 16, 4096), (2048, 768, 896),
+]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_CASES)
+def test_fp6_acc_random_codes(dev, M, N, K):
+    rng = np.random.default_rng(M * 131 + N * 7 + K)
+    a = workloads.random_weight_bytes(rng, M, K)
+    w = workloads.random_weight_bytes(rng, N, K)
+    a6, w6 = _fp6_operands(dev, a, w)
+    acc = _h(dptq.qlinear_fp6_acc(a6, w6, M, K, N))
+    ref = qlinear_acc_ref(a, 4, w)
+    bad = np.nonzero(acc.astype(np.int64) != ref)
+    assert bad[0].size == 0, f"{bad[0].size} accumulators differ, first at {bad[0][0]},{bad[1][0]}"
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_CASES[:8])
+def test_fp6_y_random_codes(dev, M, N, K):
+    rng = np.random.default_rng(M * 17 + N + K * 3)
+    a = workloads.random_weight_bytes(rng, M, K)
+    w = workloads.random_weight_bytes(rng, N, K)
+    a_s = workloads.random_scales(rng, M)
+    w_s = workloads.random_scales(rng, N)
+    a6, w6 = _fp6_operands(dev, a, w)
+    y = _h(dptq.qlinear_fp6(a6, _d(a_s, dev), w6, _d(w_s, dev), M, K, N))
+    ref = epilogue_ref(qlinear_acc_ref(a, 4, w), a_s, w_s)
+    assert np.array_equal(y.view(np.uint16), ref.view(np.uint16)), \
+        f"{(y.view(np.uint16) != ref.view(np.uint16)).sum()} outputs differ"
+
+
+@pytest.mark.parametrize("ca,cw", [(-8, -8), (7, 7), (-8, 7), (7, -8)])
+def test_fp6_extreme_accumulators(dev, ca, cw):
+    # Every code at an extreme and the largest K: |acc| = 64 K = 2^22 (the
+    # largest magnitude the fp32 accumulator must hold exactly), closed form.
+    M, N, K = 64, 32, 65536
+    nib = lambda c: (c & 15) | ((c & 15) << 4)
+    a = np.full((M, K // 2), nib(ca), dtype=np.uint8)
+    w = np.full((N, K // 2), nib(cw), dtype=np.uint8)
+    a6, w6 = _fp6_operands(dev, a, w)
+    acc = _h(dptq.qlinear_fp6_acc(a6, w6, M, K, N))
+    assert np.all(acc == ca * cw * K)
+
+
+def test_fp6_large_k_mixed(dev):
+    # A large accumulator followed by small terms: the rows hold +7 codes
+    # except a random tail, so exactness needs every low-order bit.
+    M, N, K = 96, 64, 65536
+    rng = np.random.default_rng(65536)
+    ca = np.full((M, K), 7, dtype=np.int64)
+    cw = np.full((N, K), 7, dtype=np.int64)
+    ca[:, -256:] = rng.integers(-8, 8, size=(M, 256))
+    cw[:, -256:] = rng.integers(-8, 8, size=(N, 256))
+    from oracle import pack_int4
+    a, w = pack_int4(ca), pack_int4(cw)
+    a6, w6 = _fp6_operands(dev, a, w)
+    acc = _h(dptq.qlinear_fp6_acc(a6, w6, M, K, N))
+    assert np.array_equal(acc.astype(np.int64), ca @ cw.T)
+
+
+def test_fp6_end_to_end_tiny(dev):
+    # The tiny workload (M=16, K=256, N=512, h=256) from fp16 activations and
+    # fp32 weights: rotate+quantize, pack both operands, FP6 GEMM.
+    rng = np.random.default_rng(0)
+    M, K, N, h = 16, 256, 512, 256
+    x = workloads.gauss_massive(rng, M, K)
+    w = workloads.weights(rng, N, K)
+    wp_ref, ws_ref = prepare_weights_ref(w, h)
+    c_ref, s_ref = rotate_quant_ref(x, h, 4)
+    codes, scales = dptq.rotate_quant(_d(x, dev), h, 4)
+    wp, ws = dptq.prepare_weights(_d(w, dev), h)
+    y = _h(dptq.qlinear_fp6(dptq.pack_fp6(codes), scales, dptq.pack_fp6(wp), ws, M, K, N))
+    ref = epilogue_ref(qlinear_acc_ref(c_ref, 4, wp_ref), s_ref, ws_ref)
+    assert np.array_equal(y.view(np.uint16), ref.view(np.uint16))
+
+
+FULL_SHAPES = [
+    # (name, M, K, N): LLaMA-2-7B fused QKV, LLaMA-3-8B down_proj prefill,
+    # LLaMA-2-70B qkv and down_proj prefill
+    ("llama2_7b_qkv", 2048, 4096, 12288),
+    ("llama3_8b_down", 2048, 14336, 4096),
+    ("llama2_70b_qkv", 4096, 8192, 10240),
+    ("llama2_70b_down", 4096, 28672, 8192),
+]
+
+
+@pytest.mark.parametrize("name,M,K,N", FULL_SHAPES)
+def test_fp6_full_size_vs_int8_path_and_oracle(dev, name, M, K, N):
+    g = torch.Generator(device=dev)
+    g.manual_seed(M + K + N)
+    a = torch.randint(0, 256, (M, K // 2), dtype=torch.uint8, device=dev, generator=g)
+    w = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=g)
+    a_s = torch.rand(M, device=dev, generator=g) * 1e-2 + 1e-3
+    w_s = torch.rand(N, device=dev, generator=g) * 1e-3 + 1e-4
+    a6, w6 = dptq.pack_fp6(a), dptq.pack_fp6(w)
+    y6 = dptq.qlinear_fp6(a6, a_s, w6, w_s, M, K, N)
+    y8 = dptq.qlinear(a, a_s, 4, w, w_s)
+    acc6 = dptq.qlinear_fp6_acc(a6, w6, M, K, N)
+    torch.cuda.synchronize()
+    assert torch.equal(y6.view(torch.int16), y8.view(torch.int16)), f"{name}: y differs from int8 path"
+    # sampled entries against the oracle, computed one by one
+    rng = np.random.default_rng(7)
+    rows = np.concatenate([[0, M - 1], rng.integers(0, M, 30)])
+    cols = np.concatenate([[0, N - 1], rng.integers(0, N, 30)])
+    a_h, w_h = _h(a), _h(w)
+    ref = qlinear_acc_entries(a_h, 4, w_h, rows, cols)
+    got = _h(acc6)[rows, cols].astype(np.int64)
+    assert np.array_equal(got, ref), f"{name}: sampled accumulators differ"
+    ys = _h(y6)[rows, cols]
+    y_ref = np.array([epilogue_ref(np.array([[r]]), _h(a_s)[[m]], _h(w_s)[[n]])[0, 0]
+                      for r, m, n in zip(ref, rows, cols)])
+    assert np.array_equal(ys.view(np.uint16), y_ref.view(np.uint16)), f"{name}: sampled y differs"
