@@ -6,7 +6,10 @@ activations (N(0,1) plus 4 outlier channels x50-x200) and N(0, 0.02) weights
 quantized to 4 bits per output channel.  The layer policy (Eq. 21) is looked
 up for a 32-layer model, and the step runs the layer as a non-sensitive layer
 (A4) and then as a sensitive layer (A8): per precision one rotate+quantize
-launch and one GEMM launch, all on one stream.  Inputs are resident in HBM
+launch and one GEMM launch, all on one stream.  The A4 layer runs on the FP6
+matrix cores (rotate+quantize writing the FP6 operand layout, then the FP6
+GEMM against the same weights pre-packed once); the A8 layer on the int8
+matrix cores.  Both return the oracle's results bit for bit.  Inputs are resident in HBM
 before timing; the step cycles through enough copies of activations and
 weights (> 256 MiB) that the Infinity Cache cannot hold them.
 
@@ -41,14 +44,15 @@ def parse():
                    help="token rows of the workload the CPU oracle is timed on")
     p.add_argument("--extended", action="store_true",
                    help="also time the decode shapes and the 28 x 512 rotation")
-    p.add_argument("--only", choices=["rq4", "gemm4", "rq8", "gemm8", "copy"],
+    p.add_argument("--only", choices=["rq4", "gemm4", "rq6", "gemm6", "rq8", "gemm8", "copy"],
                    help="run one kernel of the step --steps times (for counter runs) "
                         "or, with copy, a plain device copy of 256 MiB (counter calibration)")
     return p.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_prefill_a4_llama2_7b_qkv.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_prefill_a8_llama2_7b_qkv.txt")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_12487_amd", "csrc", "qgemm.hip")
+PEAK_FP6_TOPS = 10100.0      # MI355X dense fp6 / fp4 MFMA, T ops/s
 
 
 def source_digest(path):
@@ -94,9 +98,21 @@ def run_only(torch, dptq, cfg, args):
     w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
     wp, ws = dptq.prepare_weights(w, h)
     del w
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    if args.only.endswith("6"):
+        a6, s6 = dptq.rotate_quant_fp6(x, h)
+        w6 = dptq.pack_fp6(wp)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            if args.only.startswith("rq"):
+                dptq.rotate_quant_fp6(x, h, a6, s6)
+            else:
+                dptq.qlinear_fp6(a6, s6, w6, ws, M, K, N, y)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": args.only, "launches": args.steps}))
+        return
     bits = 4 if args.only.endswith("4") else 8
     codes, scales = dptq.rotate_quant(x, h, bits)
-    y = torch.empty((M, N), dtype=torch.float16, device=dev)
     torch.cuda.synchronize()
     for _ in range(args.steps):
         if args.only.startswith("rq"):
@@ -124,9 +140,10 @@ def time_layer(torch, dptq, cfg, args):
     R = max(1, args.copies)
     xs = [x.clone() for _ in range(R)]
     wps = [wp.clone() for _ in range(R)]
+    w6s = [dptq.pack_fp6(wp) for _ in range(R)]      # the same weights, FP6 operand layout
     wss = [ws.clone() for _ in range(R)]
-    codes = {4: torch.empty((M, K // 2), dtype=torch.uint8, device=dev),
-             8: torch.empty((M, K), dtype=torch.int8, device=dev)}
+    codes8 = torch.empty((M, K), dtype=torch.int8, device=dev)
+    a6 = torch.empty((dptq.fp6_bytes(M, K),), dtype=torch.uint8, device=dev)
     scales = torch.empty((M,), dtype=torch.float32, device=dev)
     y = torch.empty((M, N), dtype=torch.float16, device=dev)
     torch.cuda.synchronize()
@@ -137,8 +154,12 @@ def time_layer(torch, dptq, cfg, args):
         seq = (bits_all[n_layers // 2], bits_all[0])     # a non-sensitive, a sensitive layer
         r = i % R
         for bits in seq:
-            dptq.rotate_quant(xs[r], h, bits, codes[bits], scales)
-            dptq.qlinear(codes[bits], scales, bits, wps[r], wss[r], y)
+            if bits == 4:
+                dptq.rotate_quant_fp6(xs[r], h, a6, scales)
+                dptq.qlinear_fp6(a6, scales, w6s[r], wss[r], M, K, N, y)
+            else:
+                dptq.rotate_quant(xs[r], h, bits, codes8, scales)
+                dptq.qlinear(codes8, scales, bits, wps[r], wss[r], y)
         return seq
 
     for i in range(args.warmup):
@@ -173,9 +194,18 @@ def time_kernels(torch, dptq, cfg, args, seq, reps=24):
     R = max(1, args.copies)
     xs = [x.clone() for _ in range(R)]
     wps = [wp.clone() for _ in range(R)]
+    w6s = [dptq.pack_fp6(wp) for _ in range(R)]
     y = torch.empty((M, N), dtype=torch.float16, device=dev)
     out = {}
-    for bits in seq:
+    # the step's kernels: FP6 A4 layer, int8 A8 layer
+    a6, s6 = dptq.rotate_quant_fp6(x, h)
+    out["rotate_quant_fp6_a4"] = _graph_time(torch, [
+        (lambda i: (lambda: dptq.rotate_quant_fp6(xs[i % R], h, a6, s6)))(i) for i in range(reps)]) / 1e3
+    out["gemm_fp6_a4"] = _graph_time(torch, [
+        (lambda i: (lambda: dptq.qlinear_fp6(a6, s6, w6s[i % R], ws, M, K, N, y)))(i)
+        for i in range(reps)]) / 1e3
+    # the int8 matrix-core kernels for both precisions (A4 for comparison)
+    for bits in (8, 4):
         codes, scales = dptq.rotate_quant(x, h, bits)
         out[f"gemm_a{bits}"] = _graph_time(torch, [
             (lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
@@ -402,26 +432,40 @@ def main():
     ms_step = wall * 1e3 / args.steps
 
     per = time_kernels(torch, dptq, cfg, args, seq)
-    gemm_a4_ms = per[f"gemm_a{seq[0]}"]
-    achieved = ops_gemm / (gemm_a4_ms * 1e-3) / 1e12
-    k1_bytes = 2 * M * K + M * K * 4 // 8 + 4 * M
-    rq4_ms = per[f"rotate_quant_a{seq[0]}"]
+    step_kernels = {"rotate_quant_fp6_a4": "rq_pow2_kernel<__half, 4, false, 12, false, true>",
+                    "gemm_fp6_a4": "qgemm_fp6<false, false>",
+                    "rotate_quant_a8": "rq_pow2_kernel<__half, 8, false, 12, false, false>",
+                    "gemm_a8": "qgemm_prefill_wide<8, false>"}
+    dominant = max(step_kernels, key=lambda k: per[k])
+    dom_ms = per[dominant]
+    fp6_ms = per["gemm_fp6_a4"]
+    k1_bytes = 2 * M * K + dptq.fp6_bytes(M, K) + 4 * M
+    rq6_ms = per["rotate_quant_fp6_a4"]
+    is_fp6 = dominant == "gemm_fp6_a4"
+    dom_peak = PEAK_FP6_TOPS if is_fp6 else PEAK_INT8_TOPS
+    dom_achieved = ops_gemm / (dom_ms * 1e-3) / 1e12
     rec = {
         "metric": METRIC, "value": round(value, 3), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
         "data": "synthetic",
-        "config": {"workload": "llama2-7b fused qkv qlinear, rotate+quant+GEMM at A4 then A8",
+        "config": {"workload": "llama2-7b fused qkv qlinear, rotate+quant+GEMM at A4 (fp6 matrix "
+                               "cores) then A8 (int8 matrix cores)",
                    "M": M, "K": K, "N": N, "had_size": cfg["h"], "bits": list(seq),
                    "parallelism": "none"},
-        "roofline": {"bound": "mfma", "kernel": "qgemm_prefill_wide<4>",
-                     "achieved": round(achieved, 2), "peak": PEAK_INT8_TOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 4),
-                     "traffic": measured_traffic()},
+        "roofline": {"bound": "mfma", "kernel": step_kernels[dominant],
+                     "achieved": round(dom_achieved, 2), "peak": dom_peak,
+                     "unit": "TFLOP/s", "frac": round(dom_achieved / dom_peak, 4),
+                     "traffic": None if is_fp6 else measured_traffic()},
+        "roofline_fp6_gemm": {"bound": "mfma", "kernel": step_kernels["gemm_fp6_a4"],
+                              "achieved": round(ops_gemm / (fp6_ms * 1e-3) / 1e12, 2),
+                              "peak": PEAK_FP6_TOPS, "unit": "TFLOP/s",
+                              "frac": round(ops_gemm / (fp6_ms * 1e-3) / 1e12 / PEAK_FP6_TOPS, 4),
+                              "frac_of_int8_peak": round(ops_gemm / (fp6_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)},
         "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
-        "rotate_quant_a4": {"bound": "alu", "GB/s": round(k1_bytes / (rq4_ms * 1e-3) / 1e9, 1),
-                            "frac_of_hbm_peak": round(k1_bytes / (rq4_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "rotate_quant_fp6_a4": {"bound": "alu", "GB/s": round(k1_bytes / (rq6_ms * 1e-3) / 1e9, 1),
+                                "frac_of_hbm_peak": round(k1_bytes / (rq6_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
     }
     if args.extended:
         rec["decode"] = time_decode(torch, dptq, args)

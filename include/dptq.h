@@ -278,6 +278,20 @@ int64_t dptq_fp6_bytes(int64_t rows, int64_t K);
 int dptq_pack_fp6(const uint8_t* codes, int64_t rows, int64_t K, uint8_t* out, void* stream);
 
 /*
+ * dptq_rotate_quant_fp6 - dptq_rotate_quant at bits 4 (same rotation, scales
+ * and codes, Section 2 Eq. 4, Section 4.2) writing the codes straight into
+ * the FP6 block layout, so that no packing pass sits between the rotation
+ * and dptq_qlinear_fp6.
+ *
+ *   x, M, had_size   as for dptq_rotate_quant; K also a multiple of 128
+ *   out      device, dptq_fp6_bytes(M, K) bytes, 16-byte aligned; padding rows
+ *            of the last 32-row block are written as zero codes
+ *   a_scales device, float [M]
+ */
+int dptq_rotate_quant_fp6(const void* x, int64_t M, int64_t K, int32_t had_size, uint8_t* out,
+                          float* a_scales, void* stream);
+
+/*
  * dptq_qlinear_fp6 - dptq_qlinear at bits 4 on FP6 operands: y (fp16 [M, N])
  * from the dequant epilogue when y != NULL (a_scales, w_scales required), or
  * the raw int32 accumulators when acc != NULL (device int32 [M, N]; scales

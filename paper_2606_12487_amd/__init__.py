@@ -16,7 +16,7 @@ import os
 
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
            "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
-           "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "qlinear_fp6",
+           "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
            "qlinear_fp6_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
@@ -31,7 +31,8 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_residual_dynamics", "dptq_select_layers",
                       "dptq_kv_quant", "dptq_kv_dequant",
                       "dptq_layer_policy", "dptq_prepare_weights",
-                      "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_qlinear_fp6")
+                      "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_rotate_quant_fp6",
+                      "dptq_qlinear_fp6")
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
 GEMM_AUTO, GEMM_DECODE, GEMM_TILE_256X128, GEMM_TILE_192X256 = 0, 1, 2, 3
@@ -87,6 +88,8 @@ def lib():
         L.dptq_fp6_bytes.restype = ctypes.c_int64
         L.dptq_pack_fp6.argtypes = [vp, i64, i64, vp, vp]
         L.dptq_pack_fp6.restype = ctypes.c_int
+        L.dptq_rotate_quant_fp6.argtypes = [vp, i64, i64, i32, vp, vp, vp]
+        L.dptq_rotate_quant_fp6.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
         _lib = L
@@ -359,6 +362,26 @@ def pack_fp6(codes, out=None):
     _require(out, "out", torch.uint8, (n,))
     _check(lib().dptq_pack_fp6(_ptr(codes), R, K, _ptr(out), _stream(codes)), "dptq_pack_fp6")
     return out
+
+
+def rotate_quant_fp6(x, had_size, out=None, scales=None):
+    """Rotate and quantize fp16 rows x [M, K] at 4 bits, codes written in the
+    FP6 block layout -> (uint8 [fp6_bytes(M, K)], fp32 scales [M])."""
+    torch = _torch()
+    _require(x, "x", torch.float16)
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [M, K]")
+    M, K = x.shape
+    n = fp6_bytes(M, K)
+    if out is None:
+        out = torch.empty((n,), dtype=torch.uint8, device=x.device)
+    _require(out, "out", torch.uint8, (n,))
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=x.device)
+    _require(scales, "scales", torch.float32, (M,))
+    _check(lib().dptq_rotate_quant_fp6(_ptr(x), M, K, int(had_size), _ptr(out), _ptr(scales),
+                                       _stream(x)), "dptq_rotate_quant_fp6")
+    return out, scales
 
 
 def _fp6_args(a6, w6, M, K, N):

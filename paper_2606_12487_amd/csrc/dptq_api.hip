@@ -203,6 +203,19 @@ int dptq_pack_fp6(const uint8_t* codes, int64_t rows, int64_t K, uint8_t* out, v
   return from_hip(dptq::launch_pack_fp6(codes, rows, (int)K, out, static_cast<hipStream_t>(stream)));
 }
 
+int dptq_rotate_quant_fp6(const void* x, int64_t M, int64_t K, int32_t had_size, uint8_t* out,
+                          float* a_scales, void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(M, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (K % 128 != 0) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!x || !out || !a_scales) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(out) || !aligned16(a_scales)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_rotate_quant_fp6(x, M, (int)K, hs, out, a_scales,
+                                                static_cast<hipStream_t>(stream)));
+}
+
 int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int64_t K,
                      const uint8_t* w_fp6, const float* w_scales, int64_t N, void* y,
                      int32_t* acc, void* stream) {

@@ -20,6 +20,10 @@ constexpr int kMaxRotateK = 36864;
 hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
                                    int bits, void* codes, float* scales,
                                    hipStream_t stream);
+// Rotate + quantize at 4 bits writing the codes in the FP6 block layout
+// (padding rows of the last 32-row block are written as zero codes).
+hipError_t launch_rotate_quant_fp6(const void* x, int64_t M, int K, HadSplit hs, uint8_t* out,
+                                   float* scales, hipStream_t stream);
 hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
                                   uint8_t* w_packed, float* w_scales,
                                   hipStream_t stream);

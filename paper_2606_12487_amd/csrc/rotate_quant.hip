@@ -193,6 +193,41 @@ __device__ __forceinline__ uint32_t pack_nibbles(const uint32_t* b) {
   return (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
 }
 
+// FP6 block-layout output (4-bit codes as e2m3 values c / 2; the layout is
+// described with the FP6 GEMM).  Row m's codes k = 128 kb + 64 g + 32 s + j
+// are field j of the MFMA operand of lane 32 g + (m & 31) in half s of block
+// (kb, m / 32); its 8-byte plane c lies at byte 512 c + 8 lane of the half.
+typedef _Float16 f6_v32h __attribute__((ext_vector_type(32)));
+typedef int f6_v6i __attribute__((ext_vector_type(6)));
+
+// Byte offset of the half-block slot (plane 0) holding code k of row m.
+__device__ __forceinline__ size_t fp6_slot(int m, int k, int mblk) {
+  const int kb = k >> 7, g = (k >> 6) & 1, s = (k >> 5) & 1;
+  return ((size_t)kb * mblk + (m >> 5)) * 3072 + 1536 * s + 8 * (32 * g + (m & 31));
+}
+// c / 2 from round_bits' output word (c = the code in its low mantissa
+// bits): exact, (t + 1.5 * 2^23) / 2 - 0.75 * 2^23.
+__device__ __forceinline__ float half_code(uint32_t bits) {
+  return __builtin_fmaf(__uint_as_float(bits), 0.5f, -6291456.0f);
+}
+// Fields 0 .. N-1 of an operand from N codes (N = 16 or 32); the hardware
+// conversion packs field i at bit 6 i, exactly the layout's order, and the
+// values c / 2 are exact in e2m3.
+template <int N>
+__device__ __forceinline__ f6_v6i fp6_fields(const uint32_t* bt) {
+  f6_v32h h = {};
+#pragma unroll
+  for (int i = 0; i < N; ++i) h[i] = (_Float16)half_code(bt[i]);
+  return __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(h, 1.0f);
+}
+// Workgroup b's row when the output is the FP6 block layout: the rows of the
+// eight XCDs are contiguous ranges, so the rows of one 32-row block (whose
+// operands share cache lines) are written through one L2.
+__device__ __forceinline__ int fp6_row(int b, int mp) {
+  const int per = mp >> 3;   // mp is a multiple of 32
+  return (b & 7) * per + (b >> 3);
+}
+
 // Statistics mode (residual-dynamics calibration, Section 3.1): the kernels
 // rotate and quantize u = fl32(x + dx) and, instead of codes, write per row
 // the Jump Ratio ||dx|| / (||x|| + eps) and the historical SNR
@@ -281,9 +316,9 @@ struct Plan {
   static constexpr int width_from(int s, int left) { return (J - s + left - 1) / left; }
 };
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS>
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
 __global__ void __launch_bounds__(T)
-rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
+rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict__ codes,
                     float* __restrict__ scales, StatsArgs st) {
   extern __shared__ float lds[];
   __shared__ float red[T / 64];
@@ -291,7 +326,19 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
   float3 sums = make_float3(0.0f, 0.0f, 0.0f);
   using P = Plan<J>;
   static_assert(P::np <= 3, "pass plan too long");
-  const int row = blockIdx.x;
+  static_assert(!FP6 || BITS == 4, "FP6 output holds 4-bit codes");
+  const int mblk = (M + 31) >> 5;
+  const int row = FP6 ? fp6_row(blockIdx.x, mblk * 32) : (int)blockIdx.x;
+  if constexpr (FP6) {
+    if (row >= M) {   // padding row of the last block: zero codes
+      for (int q = threadIdx.x; q < K / 32; q += T) {
+        uint8_t* d = codes + fp6_slot(row, 32 * q, mblk);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) *reinterpret_cast<uint2*>(d + 512 * c) = make_uint2(0, 0);
+      }
+      return;
+    }
+  }
   const Tin* xr = x + (size_t)row * K;
   const int nchunk = K >> 3;
   constexpr bool load_last = (P::np == 0 && F == 1);
@@ -347,6 +394,45 @@ rotate_quant_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ code
     }
   }
 
+  if constexpr (FP6) {
+    // Each thread quantizes 8 consecutive elements (the read pattern of the
+    // 4- and 8-bit outputs); the four threads of a lane quad hold one
+    // operand's 32 codes, gather them with DPP, convert, and store one 8-byte
+    // plane each (the fourth thread has none).  K % 128 == 0 and T % 4 == 0,
+    // so quads stay together and every quad's items exist or none do.
+    for (int q0 = threadIdx.x & ~3; q0 < nchunk; q0 += T) {
+      const int q = q0 + (threadIdx.x & 3);
+      const float4* src = reinterpret_cast<const float4*>(lds + lidx(q * 8));
+      const float4 a = src[0], b = src[1];
+      const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      uint32_t hw[4];   // the 8 values c / 2 as packed fp16 pairs
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const _Float16 lo = (_Float16)half_code(round_bits(v[2 * k], sc, rc));
+        const _Float16 hi = (_Float16)half_code(round_bits(v[2 * k + 1], sc, rc));
+        hw[k] = (uint32_t)__builtin_bit_cast(unsigned short, lo) |
+                ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+      }
+      typedef unsigned int f6_v16u __attribute__((ext_vector_type(16)));
+      f6_v16u all;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        all[k] = (uint32_t)__builtin_amdgcn_mov_dpp((int)hw[k], 0x00, 0xF, 0xF, false);       // quad lane 0
+        all[4 + k] = (uint32_t)__builtin_amdgcn_mov_dpp((int)hw[k], 0x55, 0xF, 0xF, false);   // lane 1
+        all[8 + k] = (uint32_t)__builtin_amdgcn_mov_dpp((int)hw[k], 0xAA, 0xF, 0xF, false);   // lane 2
+        all[12 + k] = (uint32_t)__builtin_amdgcn_mov_dpp((int)hw[k], 0xFF, 0xF, 0xF, false);  // lane 3
+      }
+      const f6_v6i f = __builtin_amdgcn_cvt_scalef32_pk32_fp6_f16(__builtin_bit_cast(f6_v32h, all), 1.0f);
+      const int c = threadIdx.x & 3;
+      if (c < 3) {
+        uint8_t* d = codes + fp6_slot(row, 8 * q0, mblk) + 512 * c;
+        const uint32_t lo = c == 0 ? (uint32_t)f[0] : c == 1 ? (uint32_t)f[2] : (uint32_t)f[4];
+        const uint32_t hi = c == 0 ? (uint32_t)f[1] : c == 1 ? (uint32_t)f[3] : (uint32_t)f[5];
+        *reinterpret_cast<uint2*>(d) = make_uint2(lo, hi);
+      }
+    }
+    return;
+  }
   for (int q = threadIdx.x; q < nchunk; q += T) {
     const float4* src = reinterpret_cast<const float4*>(lds + lidx(q * 8));
     const float4 a = src[0], b = src[1];
@@ -375,10 +461,10 @@ size_t lds_bytes(int K) {
   return (size_t)(K + ((K + 255) >> 8) * 8) * sizeof(float);
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS>
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
 hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
                         StatsArgs st, hipStream_t stream) {
-  auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T, STATS>;
+  auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T, STATS, FP6>;
   static bool attr_set = false;
   if (!attr_set) {
     // Rows above 64 KiB of LDS need the larger dynamic allocation enabled.
@@ -388,7 +474,8 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* s
     (void)hipGetLastError();
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(T), lds_bytes(K), stream, x, K,
+  const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(T), lds_bytes(K), stream, x, (int)M, K,
                      codes, scales, st);
   return hipGetLastError();
 }
@@ -397,23 +484,23 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* s
 // rows: 256 threads, several rows per compute unit.
 constexpr int64_t kFewRows = 64;
 
-template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS>
+template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS, bool FP6>
 hipError_t launch_one(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
                       StatsArgs st, hipStream_t stream) {
   if (M <= kFewRows)
-    return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS>(x, M, K, codes, scales, st, stream);
-  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS>(x, M, K, codes, scales, st, stream);
+    return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, codes, scales, st, stream);
+  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, codes, scales, st, stream);
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int F, bool STATS, int J = 0>
+template <typename Tin, int BITS, bool WEIGHT, int F, bool STATS, bool FP6, int J = 0>
 hipError_t dispatch_j(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
                       StatsArgs st, hipStream_t stream) {
   constexpr int kMaxJ = F == 1 ? 15 : 10;   // h <= 32768
   if constexpr (J > kMaxJ) {
     return hipErrorInvalidValue;
   } else {
-    if (j == J) return launch_one<Tin, BITS, WEIGHT, F, J, STATS>(x, M, K, codes, scales, st, stream);
-    return dispatch_j<Tin, BITS, WEIGHT, F, STATS, J + 1>(j, x, M, K, codes, scales, st, stream);
+    if (j == J) return launch_one<Tin, BITS, WEIGHT, F, J, STATS, FP6>(x, M, K, codes, scales, st, stream);
+    return dispatch_j<Tin, BITS, WEIGHT, F, STATS, FP6, J + 1>(j, x, M, K, codes, scales, st, stream);
   }
 }
 
@@ -476,18 +563,30 @@ __device__ __forceinline__ float wave_max_nonneg(float m) {
   return __int_as_float(max(max(r0, r1), max(r2, r3)));
 }
 
-template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS>
+template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS, bool FP6>
 __global__ void __launch_bounds__(kThreads)
-rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
+rq_pow2_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict__ codes,
                float* __restrict__ scales, StatsArgs st) {
   static_assert(J <= 12, "segments hold 4096 elements");
+  static_assert(!FP6 || BITS == 4, "FP6 output holds 4-bit codes");
   extern __shared__ float lds[];
   __shared__ float red[kThreads / 64];
   __shared__ float red3[kThreads / 64][3];
   float3 sums = make_float3(0.0f, 0.0f, 0.0f);
-  const int row = blockIdx.x;
+  const int mblk = (M + 31) >> 5;
+  const int row = FP6 ? fp6_row(blockIdx.x, mblk * 32) : (int)blockIdx.x;
   const int t = threadIdx.x;
   const int nseg = (K + kSeg - 1) / kSeg;
+  if constexpr (FP6) {
+    if (row >= M) {   // padding row of the last block: zero codes
+      for (int q = t; q < K / 32; q += kThreads) {
+        uint8_t* d = codes + fp6_slot(row, 32 * q, mblk);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) *reinterpret_cast<uint2*>(d + 512 * c) = make_uint2(0, 0);
+      }
+      return;
+    }
+  }
   const Tin* xr = x + (size_t)row * K;
   constexpr int kLast = J <= 4 ? 1 : (J <= 8 ? 2 : 3);   // last phase with stages
   // Per-thread LDS bases of the three layouts (segment offset added per use).
@@ -595,7 +694,19 @@ rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
       bt[4 * q + 3] = round_bits(w4.w, sc, rc);
     }
     const bool full = e + 8 < K;   // else only the first 8 elements are in the row
-    if (BITS == 4) {
+    if constexpr (FP6) {
+      // 16 codes = fields 0..15 (t even) or 16..31 (t odd) of an operand:
+      // planes 0 and the low half of 1, or the high half of 1 and plane 2.
+      const f6_v6i f = fp6_fields<16>(bt);
+      uint8_t* d = codes + fp6_slot(row, e, mblk);
+      if ((e & 16) == 0) {
+        *reinterpret_cast<uint2*>(d) = make_uint2((uint32_t)f[0], (uint32_t)f[1]);
+        *reinterpret_cast<uint32_t*>(d + 512) = (uint32_t)f[2];
+      } else {
+        *reinterpret_cast<uint32_t*>(d + 516) = (uint32_t)f[0];
+        *reinterpret_cast<uint2*>(d + 1024) = make_uint2((uint32_t)f[1], (uint32_t)f[2]);
+      }
+    } else if (BITS == 4) {
       const uint32_t w[2] = {pack_nibbles(bt), pack_nibbles(bt + 8)};
       // Rows start 8-byte aligned when K % 32 == 0; otherwise word stores.
       uint32_t* dst = reinterpret_cast<uint32_t*>(codes + (size_t)row * (K / 2) + e / 2);
@@ -625,10 +736,10 @@ rq_pow2_kernel(const Tin* __restrict__ x, int K, uint8_t* __restrict__ codes,
 
 size_t pow2_lds_bytes(int K) { return (size_t)((K + kSeg - 1) / kSeg) * kSegFloats * sizeof(float); }
 
-template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS>
+template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS, bool FP6>
 hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
                        StatsArgs st, hipStream_t stream) {
-  auto kern = rq_pow2_kernel<Tin, BITS, WEIGHT, J, STATS>;
+  auto kern = rq_pow2_kernel<Tin, BITS, WEIGHT, J, STATS, FP6>;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -637,30 +748,33 @@ hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* sc
     (void)hipGetLastError();
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(kThreads), pow2_lds_bytes(K), stream, x, K,
-                     codes, scales, st);
+  const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), pow2_lds_bytes(K), stream, x,
+                     (int)M, K, codes, scales, st);
   return hipGetLastError();
 }
 
-template <typename Tin, int BITS, bool WEIGHT, bool STATS, int J = 0>
+template <typename Tin, int BITS, bool WEIGHT, bool STATS, bool FP6, int J = 0>
 hipError_t dispatch_pow2(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
                          StatsArgs st, hipStream_t stream) {
   if constexpr (J > 12) {
     return hipErrorInvalidValue;
   } else {
-    if (j == J) return launch_pow2<Tin, BITS, WEIGHT, J, STATS>(x, M, K, codes, scales, st, stream);
-    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, J + 1>(j, x, M, K, codes, scales, st, stream);
+    if (j == J) return launch_pow2<Tin, BITS, WEIGHT, J, STATS, FP6>(x, M, K, codes, scales, st, stream);
+    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, FP6, J + 1>(j, x, M, K, codes, scales, st, stream);
   }
 }
 
-template <typename Tin, int BITS, bool WEIGHT, bool STATS = false>
+template <typename Tin, int BITS, bool WEIGHT, bool STATS = false, bool FP6 = false>
 hipError_t launch_rq(const Tin* x, int64_t M, int K, HadSplit hs, uint8_t* codes,
                      float* scales, hipStream_t stream, StatsArgs st = StatsArgs{}) {
   if (M == 0) return hipSuccess;
-  if (hs.f == 28) return dispatch_j<Tin, BITS, WEIGHT, 28, STATS>(hs.j, x, M, K, codes, scales, st, stream);
+  if (hs.f == 28)
+    return dispatch_j<Tin, BITS, WEIGHT, 28, STATS, FP6>(hs.j, x, M, K, codes, scales, st, stream);
   // Up to 4096 the register-phase kernel; larger sizes the general one.
-  if (hs.j <= 12) return dispatch_pow2<Tin, BITS, WEIGHT, STATS>(hs.j, x, M, K, codes, scales, st, stream);
-  return dispatch_j<Tin, BITS, WEIGHT, 1, STATS>(hs.j, x, M, K, codes, scales, st, stream);
+  if (hs.j <= 12)
+    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, FP6>(hs.j, x, M, K, codes, scales, st, stream);
+  return dispatch_j<Tin, BITS, WEIGHT, 1, STATS, FP6>(hs.j, x, M, K, codes, scales, st, stream);
 }
 
 // Layer means of the per-token statistics (Eq. 9 and Eq. 11): one workgroup
@@ -699,6 +813,12 @@ hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
   uint8_t* c = static_cast<uint8_t*>(codes);
   if (bits == 4) return launch_rq<__half, 4, false>(xh, M, K, hs, c, scales, stream);
   return launch_rq<__half, 8, false>(xh, M, K, hs, c, scales, stream);
+}
+
+hipError_t launch_rotate_quant_fp6(const void* x, int64_t M, int K, HadSplit hs, uint8_t* out,
+                                   float* scales, hipStream_t stream) {
+  return launch_rq<__half, 4, false, false, true>(static_cast<const __half*>(x), M, K, hs, out,
+                                                  scales, stream);
 }
 
 hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,

@@ -225,3 +225,46 @@ def test_fp6_full_size_vs_int8_path_and_oracle(dev, name, M, K, N):
     y_ref = np.array([epilogue_ref(np.array([[r]]), _h(a_s)[[m]], _h(w_s)[[n]])[0, 0]
                       for r, m, n in zip(ref, rows, cols)])
     assert np.array_equal(ys.view(np.uint16), y_ref.view(np.uint16)), f"{name}: sampled y differs"
+
+
+RQ6_CASES = [
+    # (M, K, h): every kernel family (power-of-two register phases, 28 * 2^j,
+    # power of two above 4096, block-diagonal), ragged M (padding rows)
+    (1, 128, 128), (5, 256, 16), (33, 1024, 1024), (64, 4096, 4096), (70, 4096, 256),
+    (3, 14336, 28 * 512), (40, 3584, 28 * 128), (2, 8192, 8192), (31, 11008 - 11008 % 128, 128),
+    (130, 4096, 4096),
+]
+
+
+@pytest.mark.parametrize("M,K,h", RQ6_CASES)
+def test_rotate_quant_fp6_matches_oracle_codes(dev, M, K, h):
+    from oracle import pack_int4
+    rng = np.random.default_rng(M * 10 + K + h)
+    x = workloads.gauss_outliers(rng, M, K, n_channels=4)
+    out, scales = dptq.rotate_quant_fp6(_d(x, dev), h)
+    c_ref, s_ref = rotate_quant_ref(x, h, 4)
+    assert np.array_equal(_h(scales).view(np.uint32), s_ref.view(np.uint32))
+    ref = fp6_layout_ref(c_ref, K)
+    got = _h(out)
+    bad = np.nonzero(got != ref)[0]
+    assert bad.size == 0, f"{bad.size} FP6 bytes differ, first at {bad[0]}"
+
+
+def test_rotate_quant_fp6_then_gemm_bench_shape(dev):
+    # The LLaMA-2-7B fused QKV layer through the FP6 path end to end equals
+    # the int8 path (rotate_quant at 4 bits + qlinear) bit for bit.
+    rng = np.random.default_rng(1)
+    M, K, N, h = 2048, 4096, 12288, 4096
+    x = _d(workloads.gauss_outliers(rng, M, K), dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    w = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=g)
+    w_s = torch.rand(N, device=dev, generator=g) * 1e-3 + 1e-4
+    a6, s6 = dptq.rotate_quant_fp6(x, h)
+    y6 = dptq.qlinear_fp6(a6, s6, dptq.pack_fp6(w), w_s, M, K, N)
+    codes, scales = dptq.rotate_quant(x, h, 4)
+    y8 = dptq.qlinear(codes, scales, 4, w, w_s)
+    torch.cuda.synchronize()
+    assert torch.equal(s6, scales)
+    assert torch.equal(dptq.pack_fp6(codes), a6)
+    assert torch.equal(y6.view(torch.int16), y8.view(torch.int16))
