@@ -11,7 +11,9 @@ matrix cores (rotate+quantize writing the FP6 operand layout, then the FP6
 GEMM against the same weights pre-packed once); the A8 layer on the int8
 matrix cores.  Both return the oracle's results bit for bit.  Inputs are resident in HBM
 before timing; the step cycles through enough copies of activations and
-weights (> 256 MiB) that the Infinity Cache cannot hold them.
+weights (> 256 MiB) that the Infinity Cache cannot hold them.  The timed
+steps launch every kernel from the host on one stream; the same steps
+replayed from captured HIP graphs are reported under "graph".
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--extended]
 
@@ -149,10 +151,7 @@ def time_layer(torch, dptq, cfg, args):
     torch.cuda.synchronize()
 
     n_layers = 32
-    def step(i):
-        bits_all = dptq.layer_policy(n_layers)
-        seq = (bits_all[n_layers // 2], bits_all[0])     # a non-sensitive, a sensitive layer
-        r = i % R
+    def layers(r, seq):
         for bits in seq:
             if bits == 4:
                 dptq.rotate_quant_fp6(xs[r], h, a6, scales)
@@ -160,21 +159,55 @@ def time_layer(torch, dptq, cfg, args):
             else:
                 dptq.rotate_quant(xs[r], h, bits, codes8, scales)
                 dptq.qlinear(codes8, scales, bits, wps[r], wss[r], y)
-        return seq
 
+    def policy():
+        bits_all = dptq.layer_policy(n_layers)
+        return (bits_all[n_layers // 2], bits_all[0])     # a non-sensitive, a sensitive layer
+
+    # The timed steps: every kernel launched from the host on one stream.
+    seq = policy()
     for i in range(args.warmup):
-        step(i)
+        layers(i % R, policy())
     torch.cuda.synchronize()
     e0, e1 = _events(torch, 2)
     t0 = time.perf_counter()
     e0.record()
     for i in range(args.steps):
-        seq = step(i)
+        layers(i % R, policy())
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = e0.elapsed_time(e1)
-    return wall, gpu_ms, seq
+
+    # The same steps replayed from captured HIP graphs (one per input copy;
+    # the policy lookup stays on the host), for reference.  A replay must
+    # reproduce the eager result bit for bit.
+    s_cap = torch.cuda.Stream()
+    graphs = []
+    for r in range(R):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s_cap):
+            layers(r, seq)
+        graphs.append(g)
+    layers(0, seq)
+    torch.cuda.synchronize()
+    y_eager = y.clone()
+    y.zero_()
+    graphs[0].replay()
+    torch.cuda.synchronize()
+    if not torch.equal(y.view(torch.int16), y_eager.view(torch.int16)):
+        raise RuntimeError("graph replay of the step differs from its eager launches")
+    for i in range(args.warmup):
+        graphs[i % R].replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        policy()
+        graphs[i % R].replay()
+    torch.cuda.synchronize()
+    wall_graph = time.perf_counter() - t0
+    del graphs
+    return wall, gpu_ms, seq, wall_graph
 
 
 def time_kernels(torch, dptq, cfg, args, seq, reps=24):
@@ -425,7 +458,7 @@ def main():
         run_only(torch, dptq, cfg, args)
         return
 
-    wall, gpu_ms, seq = time_layer(torch, dptq, cfg, args)
+    wall, gpu_ms, seq, wall_graph = time_layer(torch, dptq, cfg, args)
     ops_gemm = 2.0 * M * N * K
     ops_step = ops_gemm * len(seq)
     value = ops_step * args.steps / wall / 1e12
@@ -463,6 +496,9 @@ def main():
                               "frac": round(ops_gemm / (fp6_ms * 1e-3) / 1e12 / PEAK_FP6_TOPS, 4),
                               "frac_of_int8_peak": round(ops_gemm / (fp6_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)},
         "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
+        "graph": {"value": round(ops_step * args.steps / wall_graph / 1e12, 3),
+                  "ms_per_step": round(wall_graph * 1e3 / args.steps, 4),
+                  "note": "the same steps replayed from captured HIP graphs"},
         "kernels_ms": {k: round(v, 4) for k, v in per.items()},
         "rotate_quant_fp6_a4": {"bound": "alu", "GB/s": round(k1_bytes / (rq6_ms * 1e-3) / 1e9, 1),
                                 "frac_of_hbm_peak": round(k1_bytes / (rq6_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},

@@ -136,17 +136,6 @@ __device__ __forceinline__ void f6_dma16(const void* sbase, uint32_t voff, uint3
                : "v"(voff), "s"(sbase), "s"(lds_off)
                : "memory", "m0");
 }
-// The same with a compile-time byte offset, which the instruction adds to the
-// global address and to the LDS address alike (so a group of loads at
-// consecutive KiB can share one base and one M0).
-template <int OFF>
-__device__ __forceinline__ void f6_dma16_off(const void* sbase, uint32_t voff, uint32_t lds_base) {
-  static_assert(OFF >= 0 && OFF < 4096, "immediate offset range");
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3"
-               :
-               : "v"(voff), "s"(sbase), "s"(lds_base), "i"(OFF)
-               : "memory", "m0");
-}
 __device__ __forceinline__ void f6_dma4(const void* sbase, uint32_t voff, uint32_t lds_off) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
                :
@@ -271,13 +260,11 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
     const uint8_t* ast = at + (size_t)kb * astride;
     const uint32_t base = smem_base + buf * C::kStage;
     if constexpr (!CLAMP) {
-      // Contiguous: groups of four loads share a base and differ in the offset.
+      // Contiguous: load q reads 1 KiB at a constant offset from the stage base.
       auto one = [&](auto qc) __attribute__((always_inline)) {
         constexpr int q = decltype(qc)::value;
         constexpr int rel = q < C::kWLoads ? q : q - C::kWLoads;
-        constexpr int grp = rel & ~3;
-        const uint8_t* src = (q < C::kWLoads ? wst : ast) + grp * 1024;
-        f6_dma16_off<(rel - grp) * 1024>(src, lane16, base + (q - (rel - grp)) * 1024);
+        f6_dma16((q < C::kWLoads ? wst : ast) + rel * 1024, lane16, base + q * 1024);
       };
       [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
         (one(std::integral_constant<int, Q0 + I>{}), ...);
