@@ -23,6 +23,8 @@ Modules
             (Section 3.1 Eq. 8-11, Section 3.3 Eq. 20).
   kv        group-wise 4-bit KV-cache quantizer and its reconstruction
             (Section 4.2, Eq. 1-2).
+  variants  the randomized-sign (QuaRot-style) rotation of Section 4.2 and
+            its weight absorption (Eq. 4-5).
 """
 
 from .hadamard import (sylvester, paley28, hadamard, split_had_size,
@@ -34,6 +36,8 @@ from .policy import layer_policy_ref
 from .residual import (jump_ratio_tokens_ref, inverse_rotate_f64, reconstructed_history_ref,
                        hist_snr_tokens_ref, residual_dynamics_ref, select_sensitive_layers_ref)
 from .kv import kv_quant_ref, kv_dequant_ref, pack_u4, unpack_u4
+from .variants import (signs_from_bits, apply_signs, rotate_quant_signed_ref,
+                       prepare_weights_signed_ref)
 
 __all__ = [
     "sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows",
@@ -44,4 +48,5 @@ __all__ = [
     "jump_ratio_tokens_ref", "inverse_rotate_f64", "reconstructed_history_ref",
     "hist_snr_tokens_ref", "residual_dynamics_ref", "select_sensitive_layers_ref",
     "kv_quant_ref", "kv_dequant_ref", "pack_u4", "unpack_u4",
+    "signs_from_bits", "apply_signs", "rotate_quant_signed_ref", "prepare_weights_signed_ref",
 ]

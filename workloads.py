@@ -168,6 +168,12 @@ def random_weight_bytes(rng, N, K):
     return rng.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
 
 
+def random_sign_bits(rng, K):
+    """Seeded random signs for the randomized rotation, as the bitmask the
+    library takes: uint8 [ceil(K/8)], bit (k & 7) of byte k >> 3 set = -1."""
+    return rng.integers(0, 256, size=((K + 7) // 8,), dtype=np.uint8)
+
+
 def random_scales(rng, n, lo=1e-4, hi=1e-1):
     """Seeded positive fp32 scales."""
     return rng.uniform(lo, hi, n).astype(np.float32)
