@@ -243,6 +243,44 @@ int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out
 int dptq_prepare_weights(const float* w, int64_t N, int64_t K, int32_t had_size,
                          uint8_t* w_packed, float* w_scales, void* stream);
 
+/* Code layouts of dptq_rotate_quant_ex. */
+typedef enum {
+  DPTQ_LAYOUT_PACKED = 0, /* the dptq_rotate_quant layout: 4-bit nibbles or int8 */
+  DPTQ_LAYOUT_FP6 = 1     /* 4-bit codes in the FP6 block layout (below) */
+} dptq_code_layout;
+
+/*
+ * dptq_rotate_quant_ex - dptq_rotate_quant with the options of the path's
+ * variants: a randomized-sign rotation and the output layout.
+ *
+ * Randomized signs (the QuaRot-style online Hadamard of Section 4.2): the
+ * rotation becomes y = (x_m * d) . B_h, the signs d_k = +-1 applied to the
+ * fp16 input before the first butterfly (exact).  Weights must be prepared
+ * with the same signs (dptq_prepare_weights_signed), which cancel in the
+ * product (Eq. 5).
+ *
+ *   signs    device, uint8 [ceil(K/8)], bit (k & 7) of byte k >> 3 set means
+ *            d_k = -1; NULL for the plain rotation (then the call equals
+ *            dptq_rotate_quant or dptq_rotate_quant_fp6)
+ *   layout   DPTQ_LAYOUT_PACKED (bits 4 or 8; out as the codes of
+ *            dptq_rotate_quant) or DPTQ_LAYOUT_FP6 (bits 4, K % 128 == 0; out
+ *            as dptq_rotate_quant_fp6, dptq_fp6_bytes(M, K) bytes)
+ *   other arguments as for dptq_rotate_quant
+ */
+int dptq_rotate_quant_ex(const void* x, int64_t M, int64_t K, int32_t had_size, int32_t bits,
+                         const uint8_t* signs, int32_t layout, void* out, float* a_scales,
+                         void* stream);
+
+/*
+ * dptq_prepare_weights_signed - dptq_prepare_weights for the randomized-sign
+ * rotation: each weight row is multiplied by the same signs d (the signs
+ * argument of dptq_rotate_quant_ex) before the rotation, so that
+ * (x D B)(W D B)^T = h X W^T (Eq. 5).  signs NULL equals dptq_prepare_weights.
+ */
+int dptq_prepare_weights_signed(const float* w, int64_t N, int64_t K, int32_t had_size,
+                                const uint8_t* signs, uint8_t* w_packed, float* w_scales,
+                                void* stream);
+
 /*
  * FP6 operand path of the 4-bit x 4-bit GEMM.  The same integer product as
  * dptq_qlinear at bits 4 (Section 2, Y = X W^T; Section 4.2 scales) computed

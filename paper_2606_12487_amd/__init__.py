@@ -17,6 +17,7 @@ import os
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
            "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
            "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
+           "LAYOUT_PACKED", "LAYOUT_FP6",
            "qlinear_fp6_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
@@ -32,7 +33,10 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_kv_quant", "dptq_kv_dequant",
                       "dptq_layer_policy", "dptq_prepare_weights",
                       "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_rotate_quant_fp6",
-                      "dptq_qlinear_fp6")
+                      "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed")
+
+# Code layouts of dptq_rotate_quant_ex.
+LAYOUT_PACKED, LAYOUT_FP6 = 0, 1
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
 GEMM_AUTO, GEMM_DECODE, GEMM_TILE_256X128, GEMM_TILE_192X256 = 0, 1, 2, 3
@@ -90,6 +94,10 @@ def lib():
         L.dptq_pack_fp6.restype = ctypes.c_int
         L.dptq_rotate_quant_fp6.argtypes = [vp, i64, i64, i32, vp, vp, vp]
         L.dptq_rotate_quant_fp6.restype = ctypes.c_int
+        L.dptq_rotate_quant_ex.argtypes = [vp, i64, i64, i32, i32, vp, i32, vp, vp, vp]
+        L.dptq_rotate_quant_ex.restype = ctypes.c_int
+        L.dptq_prepare_weights_signed.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
+        L.dptq_prepare_weights_signed.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
         _lib = L
@@ -144,8 +152,18 @@ def code_shape(M, K, bits):
     return (M, K // 2) if bits == 4 else (M, K)
 
 
-def rotate_quant(x, had_size, bits, codes=None, scales=None):
-    """Rotate (I (x) H_h) and quantize fp16 rows x [M, K] -> (codes, fp32 scales [M])."""
+def _signs_arg(signs, K, dev):
+    if signs is None:
+        return None
+    _require(signs, "signs", _torch().uint8, ((K + 7) // 8,))
+    if signs.device != dev:
+        raise ValueError("signs must be on the same device as x")
+    return signs
+
+
+def rotate_quant(x, had_size, bits, codes=None, scales=None, signs=None):
+    """Rotate (I (x) H_h) and quantize fp16 rows x [M, K] -> (codes, fp32 scales [M]).
+    signs: optional uint8 bitmask [ceil(K/8)] of randomized signs (bit set = -1)."""
     torch = _torch()
     _require(x, "x", torch.float16)
     if x.dim() != 2:
@@ -160,8 +178,14 @@ def rotate_quant(x, had_size, bits, codes=None, scales=None):
     if scales is None:
         scales = torch.empty((M,), dtype=torch.float32, device=x.device)
     _require(scales, "scales", torch.float32, (M,))
-    _check(lib().dptq_rotate_quant(_ptr(x), M, K, int(had_size), int(bits), _ptr(codes),
-                                   _ptr(scales), _stream(x)), "dptq_rotate_quant")
+    signs = _signs_arg(signs, K, x.device)
+    if signs is None:
+        _check(lib().dptq_rotate_quant(_ptr(x), M, K, int(had_size), int(bits), _ptr(codes),
+                                       _ptr(scales), _stream(x)), "dptq_rotate_quant")
+    else:
+        _check(lib().dptq_rotate_quant_ex(_ptr(x), M, K, int(had_size), int(bits), _ptr(signs),
+                                          LAYOUT_PACKED, _ptr(codes), _ptr(scales), _stream(x)),
+               "dptq_rotate_quant_ex")
     return codes, scales
 
 
@@ -322,8 +346,9 @@ def layer_policy(num_layers, mask=None):
     return [int(v) for v in out[:L]]
 
 
-def prepare_weights(w, had_size, w_packed=None, w_scales=None):
-    """Offline: rotate, quantize to 4 bits per output channel and pack fp32 w [N, K]."""
+def prepare_weights(w, had_size, w_packed=None, w_scales=None, signs=None):
+    """Offline: rotate, quantize to 4 bits per output channel and pack fp32 w [N, K].
+    signs: the randomized-sign bitmask of the activations' rotation, if any."""
     torch = _torch()
     _require(w, "w", torch.float32)
     if w.dim() != 2:
@@ -335,8 +360,14 @@ def prepare_weights(w, had_size, w_packed=None, w_scales=None):
     if w_scales is None:
         w_scales = torch.empty((N,), dtype=torch.float32, device=w.device)
     _require(w_scales, "w_scales", torch.float32, (N,))
-    _check(lib().dptq_prepare_weights(_ptr(w), N, K, int(had_size), _ptr(w_packed),
-                                      _ptr(w_scales), _stream(w)), "dptq_prepare_weights")
+    signs = _signs_arg(signs, K, w.device)
+    if signs is None:
+        _check(lib().dptq_prepare_weights(_ptr(w), N, K, int(had_size), _ptr(w_packed),
+                                          _ptr(w_scales), _stream(w)), "dptq_prepare_weights")
+    else:
+        _check(lib().dptq_prepare_weights_signed(_ptr(w), N, K, int(had_size), _ptr(signs),
+                                                 _ptr(w_packed), _ptr(w_scales), _stream(w)),
+               "dptq_prepare_weights_signed")
     return w_packed, w_scales
 
 
@@ -364,7 +395,7 @@ def pack_fp6(codes, out=None):
     return out
 
 
-def rotate_quant_fp6(x, had_size, out=None, scales=None):
+def rotate_quant_fp6(x, had_size, out=None, scales=None, signs=None):
     """Rotate and quantize fp16 rows x [M, K] at 4 bits, codes written in the
     FP6 block layout -> (uint8 [fp6_bytes(M, K)], fp32 scales [M])."""
     torch = _torch()
@@ -379,8 +410,14 @@ def rotate_quant_fp6(x, had_size, out=None, scales=None):
     if scales is None:
         scales = torch.empty((M,), dtype=torch.float32, device=x.device)
     _require(scales, "scales", torch.float32, (M,))
-    _check(lib().dptq_rotate_quant_fp6(_ptr(x), M, K, int(had_size), _ptr(out), _ptr(scales),
-                                       _stream(x)), "dptq_rotate_quant_fp6")
+    signs = _signs_arg(signs, K, x.device)
+    if signs is None:
+        _check(lib().dptq_rotate_quant_fp6(_ptr(x), M, K, int(had_size), _ptr(out), _ptr(scales),
+                                           _stream(x)), "dptq_rotate_quant_fp6")
+    else:
+        _check(lib().dptq_rotate_quant_ex(_ptr(x), M, K, int(had_size), 4, _ptr(signs), LAYOUT_FP6,
+                                          _ptr(out), _ptr(scales), _stream(x)),
+               "dptq_rotate_quant_ex")
     return out, scales
 
 

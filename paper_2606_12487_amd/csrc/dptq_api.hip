@@ -216,6 +216,39 @@ int dptq_rotate_quant_fp6(const void* x, int64_t M, int64_t K, int32_t had_size,
                                                 static_cast<hipStream_t>(stream)));
 }
 
+int dptq_rotate_quant_ex(const void* x, int64_t M, int64_t K, int32_t had_size, int32_t bits,
+                         const uint8_t* signs, int32_t layout, void* out, float* a_scales,
+                         void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(M, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (bits != 4 && bits != 8) return DPTQ_ERR_INVALID_ARG;
+  if (layout != DPTQ_LAYOUT_PACKED && layout != DPTQ_LAYOUT_FP6) return DPTQ_ERR_INVALID_ARG;
+  if (layout == DPTQ_LAYOUT_FP6 && bits != 4) return DPTQ_ERR_INVALID_ARG;
+  if (layout == DPTQ_LAYOUT_FP6 && K % 128 != 0) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!x || !out || !a_scales) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(out) || !aligned16(a_scales)) return DPTQ_ERR_INVALID_ARG;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (layout == DPTQ_LAYOUT_FP6)
+    return from_hip(dptq::launch_rotate_quant_fp6(x, M, (int)K, hs, static_cast<uint8_t*>(out),
+                                                  a_scales, s, signs));
+  return from_hip(dptq::launch_rotate_quant_signed(x, M, (int)K, hs, bits, signs, out, a_scales, s));
+}
+
+int dptq_prepare_weights_signed(const float* w, int64_t N, int64_t K, int32_t had_size,
+                                const uint8_t* signs, uint8_t* w_packed, float* w_scales,
+                                void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(N, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (N == 0) return DPTQ_OK;
+  if (!w || !w_packed || !w_scales) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(w) || !aligned16(w_packed) || !aligned16(w_scales)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_prepare_weights(w, N, (int)K, hs, w_packed, w_scales,
+                                               static_cast<hipStream_t>(stream), signs));
+}
+
 int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int64_t K,
                      const uint8_t* w_fp6, const float* w_scales, int64_t N, void* y,
                      int32_t* acc, void* stream) {

@@ -23,10 +23,16 @@ hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
 // Rotate + quantize at 4 bits writing the codes in the FP6 block layout
 // (padding rows of the last 32-row block are written as zero codes).
 hipError_t launch_rotate_quant_fp6(const void* x, int64_t M, int K, HadSplit hs, uint8_t* out,
-                                   float* scales, hipStream_t stream);
+                                   float* scales, hipStream_t stream,
+                                   const uint8_t* signs = nullptr);
+// signs (optional, nullptr = none): randomized-sign bitmask over K, bit
+// (k & 7) of byte k >> 3 set = negate element k before the rotation.
 hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
                                   uint8_t* w_packed, float* w_scales,
-                                  hipStream_t stream);
+                                  hipStream_t stream, const uint8_t* signs = nullptr);
+hipError_t launch_rotate_quant_signed(const void* x, int64_t M, int K, HadSplit hs, int bits,
+                                      const uint8_t* signs, void* codes, float* scales,
+                                      hipStream_t stream);
 // Residual-dynamics statistics of x + dx (statistics mode of the rotate+quantize
 // kernels): per-row Jump Ratio and historical SNR (dB), and their means when
 // means != nullptr.

@@ -93,6 +93,14 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
   v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
+// Randomized signs (bit set = negate) of N consecutive elements, from their
+// bitmask bits m (bit r for element r): a sign-bit flip, exact.
+template <int N>
+__device__ __forceinline__ void apply_sign_bits(float* v, uint32_t m) {
+#pragma unroll
+  for (int r = 0; r < N; ++r) v[r] = __uint_as_float(__float_as_uint(v[r]) ^ (((m >> r) & 1u) << 31));
+}
+
 __device__ __forceinline__ float absmax8(const float* v, float m) {
 #pragma unroll
   for (int k = 0; k < 8; ++k) m = fmaxf(m, fabsf(v[k]));
@@ -318,8 +326,8 @@ struct Plan {
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
 __global__ void __launch_bounds__(T)
-rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict__ codes,
-                    float* __restrict__ scales, StatsArgs st) {
+rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __restrict__ signs,
+                    uint8_t* __restrict__ codes, float* __restrict__ scales, StatsArgs st) {
   extern __shared__ float lds[];
   __shared__ float red[T / 64];
   __shared__ float red3[T / 64][3];
@@ -346,8 +354,12 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict
   float tmax = 0.0f;
   for (int q = threadIdx.x; q < nchunk; q += T) {
     float v[8];
-    if constexpr (STATS) load8_sum(xr + (size_t)q * 8, st.dx + (size_t)row * K + (size_t)q * 8, v, sums.x, sums.y);
-    else load8(xr + (size_t)q * 8, v);
+    if constexpr (STATS) {
+      load8_sum(xr + (size_t)q * 8, st.dx + (size_t)row * K + (size_t)q * 8, v, sums.x, sums.y);
+    } else {
+      load8(xr + (size_t)q * 8, v);
+      if (signs) apply_sign_bits<8>(v, signs[q]);
+    }
     butterflies<3>(v, 0, P::j0);
     if (load_last) tmax = absmax8(v, tmax);
     float4* d = reinterpret_cast<float4*>(lds + lidx(q * 8));
@@ -462,8 +474,8 @@ size_t lds_bytes(int K) {
 }
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
-hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                        StatsArgs st, hipStream_t stream) {
+hipError_t launch_one_t(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
+                        float* scales, StatsArgs st, hipStream_t stream) {
   auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T, STATS, FP6>;
   static bool attr_set = false;
   if (!attr_set) {
@@ -476,7 +488,7 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* s
   }
   const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(T), lds_bytes(K), stream, x, (int)M, K,
-                     codes, scales, st);
+                     signs, codes, scales, st);
   return hipGetLastError();
 }
 
@@ -485,22 +497,26 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, uint8_t* codes, float* s
 constexpr int64_t kFewRows = 64;
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS, bool FP6>
-hipError_t launch_one(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                      StatsArgs st, hipStream_t stream) {
+hipError_t launch_one(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
+                      float* scales, StatsArgs st, hipStream_t stream) {
   if (M <= kFewRows)
-    return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, codes, scales, st, stream);
-  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, codes, scales, st, stream);
+    return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, signs, codes, scales, st,
+                                                                  stream);
+  return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, signs, codes, scales,
+                                                                    st, stream);
 }
 
 template <typename Tin, int BITS, bool WEIGHT, int F, bool STATS, bool FP6, int J = 0>
-hipError_t dispatch_j(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                      StatsArgs st, hipStream_t stream) {
+hipError_t dispatch_j(int j, const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
+                      float* scales, StatsArgs st, hipStream_t stream) {
   constexpr int kMaxJ = F == 1 ? 15 : 10;   // h <= 32768
   if constexpr (J > kMaxJ) {
     return hipErrorInvalidValue;
   } else {
-    if (j == J) return launch_one<Tin, BITS, WEIGHT, F, J, STATS, FP6>(x, M, K, codes, scales, st, stream);
-    return dispatch_j<Tin, BITS, WEIGHT, F, STATS, FP6, J + 1>(j, x, M, K, codes, scales, st, stream);
+    if (j == J)
+      return launch_one<Tin, BITS, WEIGHT, F, J, STATS, FP6>(x, M, K, signs, codes, scales, st, stream);
+    return dispatch_j<Tin, BITS, WEIGHT, F, STATS, FP6, J + 1>(j, x, M, K, signs, codes, scales, st,
+                                                               stream);
   }
 }
 
@@ -565,8 +581,8 @@ __device__ __forceinline__ float wave_max_nonneg(float m) {
 
 template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS, bool FP6>
 __global__ void __launch_bounds__(kThreads)
-rq_pow2_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict__ codes,
-               float* __restrict__ scales, StatsArgs st) {
+rq_pow2_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __restrict__ signs,
+               uint8_t* __restrict__ codes, float* __restrict__ scales, StatsArgs st) {
   static_assert(J <= 12, "segments hold 4096 elements");
   static_assert(!FP6 || BITS == 4, "FP6 output holds 4-bit codes");
   extern __shared__ float lds[];
@@ -614,6 +630,11 @@ rq_pow2_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict__ co
     } else {
 #pragma unroll
       for (int r = 8; r < 16; ++r) v[r] = 0.0f;
+    }
+    if (!STATS && signs) {
+      const uint32_t m = (e < K ? (uint32_t)signs[e / 8] : 0u) |
+                         (e + 8 < K ? (uint32_t)signs[e / 8 + 1] << 8 : 0u);
+      apply_sign_bits<16>(v, m);
     }
     stages16<0, (J < 4 ? J : 4)>(v);
     if (kLast == 1) tmax = absmax16(v, tmax);
@@ -737,8 +758,8 @@ rq_pow2_kernel(const Tin* __restrict__ x, int M, int K, uint8_t* __restrict__ co
 size_t pow2_lds_bytes(int K) { return (size_t)((K + kSeg - 1) / kSeg) * kSegFloats * sizeof(float); }
 
 template <typename Tin, int BITS, bool WEIGHT, int J, bool STATS, bool FP6>
-hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                       StatsArgs st, hipStream_t stream) {
+hipError_t launch_pow2(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
+                       float* scales, StatsArgs st, hipStream_t stream) {
   auto kern = rq_pow2_kernel<Tin, BITS, WEIGHT, J, STATS, FP6>;
   static bool attr_set = false;
   if (!attr_set) {
@@ -750,31 +771,39 @@ hipError_t launch_pow2(const Tin* x, int64_t M, int K, uint8_t* codes, float* sc
   }
   const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), pow2_lds_bytes(K), stream, x,
-                     (int)M, K, codes, scales, st);
+                     (int)M, K, signs, codes, scales, st);
   return hipGetLastError();
 }
 
 template <typename Tin, int BITS, bool WEIGHT, bool STATS, bool FP6, int J = 0>
-hipError_t dispatch_pow2(int j, const Tin* x, int64_t M, int K, uint8_t* codes, float* scales,
-                         StatsArgs st, hipStream_t stream) {
+hipError_t dispatch_pow2(int j, const Tin* x, int64_t M, int K, const uint8_t* signs,
+                         uint8_t* codes, float* scales, StatsArgs st, hipStream_t stream) {
   if constexpr (J > 12) {
     return hipErrorInvalidValue;
   } else {
-    if (j == J) return launch_pow2<Tin, BITS, WEIGHT, J, STATS, FP6>(x, M, K, codes, scales, st, stream);
-    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, FP6, J + 1>(j, x, M, K, codes, scales, st, stream);
+    if (j == J)
+      return launch_pow2<Tin, BITS, WEIGHT, J, STATS, FP6>(x, M, K, signs, codes, scales, st, stream);
+    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, FP6, J + 1>(j, x, M, K, signs, codes, scales, st,
+                                                               stream);
   }
 }
 
+// signs: optional randomized-sign bitmask (bit set = negate the element
+// before the rotation); nullptr for the plain rotation.
 template <typename Tin, int BITS, bool WEIGHT, bool STATS = false, bool FP6 = false>
 hipError_t launch_rq(const Tin* x, int64_t M, int K, HadSplit hs, uint8_t* codes,
-                     float* scales, hipStream_t stream, StatsArgs st = StatsArgs{}) {
+                     float* scales, hipStream_t stream, StatsArgs st = StatsArgs{},
+                     const uint8_t* signs = nullptr) {
   if (M == 0) return hipSuccess;
   if (hs.f == 28)
-    return dispatch_j<Tin, BITS, WEIGHT, 28, STATS, FP6>(hs.j, x, M, K, codes, scales, st, stream);
+    return dispatch_j<Tin, BITS, WEIGHT, 28, STATS, FP6>(hs.j, x, M, K, signs, codes, scales, st,
+                                                          stream);
   // Up to 4096 the register-phase kernel; larger sizes the general one.
   if (hs.j <= 12)
-    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, FP6>(hs.j, x, M, K, codes, scales, st, stream);
-  return dispatch_j<Tin, BITS, WEIGHT, 1, STATS, FP6>(hs.j, x, M, K, codes, scales, st, stream);
+    return dispatch_pow2<Tin, BITS, WEIGHT, STATS, FP6>(hs.j, x, M, K, signs, codes, scales, st,
+                                                        stream);
+  return dispatch_j<Tin, BITS, WEIGHT, 1, STATS, FP6>(hs.j, x, M, K, signs, codes, scales, st,
+                                                       stream);
 }
 
 // Layer means of the per-token statistics (Eq. 9 and Eq. 11): one workgroup
@@ -816,15 +845,24 @@ hipError_t launch_rotate_quant_f16(const void* x, int64_t M, int K, HadSplit hs,
 }
 
 hipError_t launch_rotate_quant_fp6(const void* x, int64_t M, int K, HadSplit hs, uint8_t* out,
-                                   float* scales, hipStream_t stream) {
+                                   float* scales, hipStream_t stream, const uint8_t* signs) {
   return launch_rq<__half, 4, false, false, true>(static_cast<const __half*>(x), M, K, hs, out,
-                                                  scales, stream);
+                                                  scales, stream, StatsArgs{}, signs);
+}
+
+hipError_t launch_rotate_quant_signed(const void* x, int64_t M, int K, HadSplit hs, int bits,
+                                      const uint8_t* signs, void* codes, float* scales,
+                                      hipStream_t stream) {
+  const __half* xh = static_cast<const __half*>(x);
+  uint8_t* c = static_cast<uint8_t*>(codes);
+  if (bits == 4) return launch_rq<__half, 4, false>(xh, M, K, hs, c, scales, stream, StatsArgs{}, signs);
+  return launch_rq<__half, 8, false>(xh, M, K, hs, c, scales, stream, StatsArgs{}, signs);
 }
 
 hipError_t launch_prepare_weights(const float* w, int64_t N, int K, HadSplit hs,
                                   uint8_t* w_packed, float* w_scales,
-                                  hipStream_t stream) {
-  return launch_rq<float, 4, true>(w, N, K, hs, w_packed, w_scales, stream);
+                                  hipStream_t stream, const uint8_t* signs) {
+  return launch_rq<float, 4, true>(w, N, K, hs, w_packed, w_scales, stream, StatsArgs{}, signs);
 }
 
 hipError_t launch_residual_stats(const void* x, const void* dx, int64_t T, int K, HadSplit hs,

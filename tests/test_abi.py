@@ -227,3 +227,31 @@ def test_python_wrappers_check_tensors():
         dptq.rotate_quant(torch.zeros(4, 256, dtype=torch.float16), 256, 4)  # not on GPU
     with pytest.raises(ValueError):
         dptq.layer_policy(3, [1, 0])
+
+
+def test_rotate_quant_ex_validation(L):
+    def call(bits=4, layout=0, K=256, h=256, x=FAKE, out=FAKE, sc=FAKE, M=4):
+        return L.dptq_rotate_quant_ex(x, M, K, h, bits, NULL, layout, out, sc, NULL)
+    assert call(layout=2) == INVALID
+    assert call(layout=1, bits=8) == INVALID
+    assert call(layout=1, K=64, h=64) == UNSUPPORTED          # FP6 layout needs K % 128 == 0
+    assert call(bits=5) == INVALID
+    assert call(x=NULL) == INVALID
+    assert call(out=MISALIGNED) == INVALID
+    assert call(M=0, x=NULL) == OK                            # nothing to do, nothing enqueued
+    assert L.dptq_prepare_weights_signed(FAKE, 4, 256, 100, NULL, FAKE, FAKE, NULL) == INVALID
+    assert L.dptq_prepare_weights_signed(NULL, 4, 256, 256, NULL, FAKE, FAKE, NULL) == INVALID
+
+
+def test_fp6_entry_points_validation(L):
+    assert L.dptq_fp6_bytes(32, 128) == 3072
+    assert L.dptq_fp6_bytes(33, 256) == 2 * 2 * 3072
+    assert L.dptq_fp6_bytes(1, 100) == -1
+    assert L.dptq_pack_fp6(FAKE, 4, 192, FAKE, NULL) == UNSUPPORTED
+    assert L.dptq_pack_fp6(MISALIGNED, 4, 256, FAKE, NULL) == INVALID
+    # exactly one of y and acc
+    assert L.dptq_qlinear_fp6(FAKE, FAKE, 4, 256, FAKE, FAKE, 32, NULL, NULL, NULL) == INVALID
+    assert L.dptq_qlinear_fp6(FAKE, FAKE, 4, 256, FAKE, FAKE, 32, FAKE, FAKE, NULL) == INVALID
+    assert L.dptq_qlinear_fp6(FAKE, FAKE, 4, 200, FAKE, FAKE, 32, FAKE, NULL, NULL) == UNSUPPORTED
+    assert L.dptq_qlinear_fp6(FAKE, FAKE, 4, 256, FAKE, FAKE, 24, FAKE, NULL, NULL) == UNSUPPORTED
+    assert L.dptq_rotate_quant_fp6(FAKE, 4, 192, 64, FAKE, FAKE, NULL) == UNSUPPORTED
