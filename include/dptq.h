@@ -139,6 +139,29 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
                         int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream);
 
 /*
+ * dptq_qlinear_decode_fused - a decode-shape quantized linear in one launch:
+ * dptq_rotate_quant followed by dptq_qlinear for M <= 16 tokens (Eq. 4, Eq. 2,
+ * Section 2 Y = X W^T, Section 4.2 scales; the decode stage of Section 4.9),
+ * with the same results bit for bit.  The rotation of the M rows overlaps
+ * with the start of the weight stream instead of being a launch of its own.
+ *
+ *   x, M, K, had_size, bits   as for dptq_rotate_quant; 1 <= M <= 16 (M = 0
+ *            enqueues nothing), K a multiple of 128 and <= 32768
+ *   w_packed, w_scales, N, y  as for dptq_qlinear
+ *   codes    device, the activation codes (dptq_rotate_quant layout), written
+ *   a_scales device, float [M], written
+ *   sync     device, int32 [4], 16-byte aligned, zero before the first call;
+ *            the call leaves sync[0], sync[1] zero again.  sync[2] != 0 reports
+ *            that a workgroup gave up waiting for the codes (not expected; the
+ *            outputs of that call are then unspecified); clear it to reuse.
+ *            Calls that share a sync buffer must not overlap in time.
+ */
+int dptq_qlinear_decode_fused(const void* x, int64_t M, int64_t K, int32_t had_size,
+                              int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                              int64_t N, void* y, void* codes, float* a_scales, int32_t* sync,
+                              void* stream);
+
+/*
  * dptq_residual_dynamics - residual-dynamics calibration statistics of one
  * layer (Section 3.1 Eq. 8-11; quantization in the rotated space, Section 3.2
  * Eq. 14-16).  For every token row t of the residual state x entering the

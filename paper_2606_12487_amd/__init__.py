@@ -17,7 +17,7 @@ import os
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
            "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
            "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
-           "LAYOUT_PACKED", "LAYOUT_FP6",
+           "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "new_sync",
            "qlinear_fp6_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
@@ -33,7 +33,8 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_kv_quant", "dptq_kv_dequant",
                       "dptq_layer_policy", "dptq_prepare_weights",
                       "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_rotate_quant_fp6",
-                      "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed")
+                      "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed",
+                      "dptq_qlinear_decode_fused")
 
 # Code layouts of dptq_rotate_quant_ex.
 LAYOUT_PACKED, LAYOUT_FP6 = 0, 1
@@ -98,6 +99,9 @@ def lib():
         L.dptq_rotate_quant_ex.restype = ctypes.c_int
         L.dptq_prepare_weights_signed.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
         L.dptq_prepare_weights_signed.restype = ctypes.c_int
+        L.dptq_qlinear_decode_fused.argtypes = [vp, i64, i64, i32, i32, vp, vp, i64, vp, vp, vp,
+                                                 vp, vp]
+        L.dptq_qlinear_decode_fused.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
         _lib = L
@@ -452,3 +456,35 @@ def qlinear_fp6_acc(a6, w6, M, K, N, acc=None):
     _check(lib().dptq_qlinear_fp6(_ptr(a6), None, M, K, _ptr(w6), None, N, None, _ptr(acc),
                                   _stream(a6)), "dptq_qlinear_fp6")
     return acc
+
+
+def new_sync(device):
+    """A zeroed int32 [4] sync buffer for qlinear_decode_fused (reusable)."""
+    return _torch().zeros((4,), dtype=_torch().int32, device=device)
+
+
+def qlinear_decode_fused(x, had_size, bits, w_packed, w_scales, sync, y=None, codes=None,
+                         scales=None):
+    """Decode-shape (M <= 16) rotate + quantize + GEMM in one launch.
+    Returns (y [M, N] fp16, codes, scales); sync from new_sync()."""
+    torch = _torch()
+    _require(x, "x", torch.float16)
+    M, K = x.shape
+    N = w_packed.shape[0]
+    _require(w_packed, "w_packed", torch.uint8, (N, K // 2))
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    _require(sync, "sync", torch.int32, (4,))
+    cdt = torch.uint8 if bits == 4 else torch.int8
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    if codes is None:
+        codes = torch.empty(code_shape(M, K, bits), dtype=cdt, device=x.device)
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=x.device)
+    _require(y, "y", torch.float16, (M, N))
+    _require(codes, "codes", cdt, code_shape(M, K, bits))
+    _require(scales, "scales", torch.float32, (M,))
+    _check(lib().dptq_qlinear_decode_fused(_ptr(x), M, K, int(had_size), int(bits), _ptr(w_packed),
+                                           _ptr(w_scales), N, _ptr(y), _ptr(codes), _ptr(scales),
+                                           _ptr(sync), _stream(x)), "dptq_qlinear_decode_fused")
+    return y, codes, scales

@@ -270,6 +270,25 @@ int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int
                                            static_cast<hipStream_t>(stream)));
 }
 
+int dptq_qlinear_decode_fused(const void* x, int64_t M, int64_t K, int32_t had_size,
+                              int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                              int64_t N, void* y, void* codes, float* a_scales, int32_t* sync,
+                              void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(M, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  st = check_gemm_shape(M, K, bits, N);
+  if (st != DPTQ_OK) return st;
+  if (M > 16 || K > dptq::kMaxFusedK) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!x || !w_packed || !w_scales || !y || !codes || !a_scales || !sync) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(w_packed) || !aligned16(w_scales) || !aligned16(y) ||
+      !aligned16(codes) || !aligned4(a_scales) || !aligned16(sync))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_decode_fused(x, M, (int)K, hs, bits, w_packed, w_scales, N, y, codes,
+                                            a_scales, sync, static_cast<hipStream_t>(stream)));
+}
+
 int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {
   if (num_layers < 1 || !bits_out) return DPTQ_ERR_INVALID_ARG;
   for (int32_t l = 0; l < num_layers; ++l) {

@@ -59,6 +59,17 @@ hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
                           const float* w_scales, int64_t N, void* y,
                           int32_t* out_acc, int kernel, hipStream_t stream);
 
+// Largest K of the fused decode kernel (its row staging plus the GEMM's
+// partial tiles fit in 160 KiB of LDS).
+constexpr int kMaxFusedK = 32768;
+// Decode-shape (M <= 16) rotate + quantize + GEMM + epilogue in one launch;
+// codes / a_scales receive the activation codes and scales; sync is the
+// caller's int32 [4] (zero before the first call, zero again after each call;
+// sync[2] != 0 reports a wait that gave up).
+hipError_t launch_decode_fused(const void* x, int64_t M, int K, HadSplit hs, int bits,
+                               const uint8_t* w_packed, const float* w_scales, int64_t N, void* y,
+                               void* codes, float* a_scales, int32_t* sync, hipStream_t stream);
+
 // Compute units of the current device (cached per device).
 int device_cus();
 

@@ -255,3 +255,17 @@ def test_fp6_entry_points_validation(L):
     assert L.dptq_qlinear_fp6(FAKE, FAKE, 4, 200, FAKE, FAKE, 32, FAKE, NULL, NULL) == UNSUPPORTED
     assert L.dptq_qlinear_fp6(FAKE, FAKE, 4, 256, FAKE, FAKE, 24, FAKE, NULL, NULL) == UNSUPPORTED
     assert L.dptq_rotate_quant_fp6(FAKE, 4, 192, 64, FAKE, FAKE, NULL) == UNSUPPORTED
+
+
+def test_fused_decode_validation(L):
+    def call(M=4, K=4096, h=4096, bits=4, N=64, sync=FAKE, x=FAKE):
+        return L.dptq_qlinear_decode_fused(x, M, K, h, bits, FAKE, FAKE, N, FAKE, FAKE, FAKE,
+                                           sync, NULL)
+    assert call(M=17) == UNSUPPORTED            # decode shapes only
+    assert call(K=36864, h=4096) == UNSUPPORTED # larger than the fused kernel's row staging
+    assert call(bits=6) == INVALID
+    assert call(sync=NULL) == INVALID
+    assert call(sync=MISALIGNED) == INVALID
+    assert call(N=24) == UNSUPPORTED
+    assert call(h=3) == INVALID
+    assert call(M=0, x=NULL) == OK

@@ -102,3 +102,52 @@ def test_signed_layer_end_to_end(dev, bits):
         a6, s6 = dptq.rotate_quant_fp6(_d(x, dev), h, signs=sd)
         y6 = _h(dptq.qlinear_fp6(a6, s6, dptq.pack_fp6(wp), ws, M, K, N))
         assert np.array_equal(y6.view(np.uint16), y_ref.view(np.uint16))
+
+
+FUSED_CASES = [
+    # (M, K, N, h, bits): LLaMA decode shapes (7B QKV, 8B down with h = 28 x 512,
+    # 7B down with 43 blocks of 256, 70B QKV at h = 8192), the tiny workload,
+    # and grids smaller than M (a workgroup produces several rows)
+    (1, 4096, 12288, 4096, 4), (4, 14336, 4096, 28 * 512, 4), (16, 256, 512, 256, 8),
+    (8, 11008, 4096, 256, 4), (8, 8192, 1024, 8192, 8), (3, 512, 32, 512, 4),
+    (16, 1024, 16, 1024, 8), (16, 4096, 12288, 4096, 8),
+]
+
+
+@pytest.mark.parametrize("M,K,N,h,bits", FUSED_CASES)
+def test_fused_decode_matches_oracle(dev, M, K, N, h, bits):
+    from oracle import rotate_quant_ref, prepare_weights_ref
+    rng = np.random.default_rng(M * 31 + K + N + bits)
+    x = workloads.student_t(rng, M, K) if h % 28 == 0 else workloads.gauss_outliers(rng, M, K)
+    wp = workloads.random_weight_bytes(rng, N, K)
+    ws = workloads.random_scales(rng, N)
+    c_ref, s_ref = rotate_quant_ref(x, h, bits)
+    y_ref = epilogue_ref(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
+    sync = dptq.new_sync(dev)
+    y, codes, scales = dptq.qlinear_decode_fused(_d(x, dev), h, bits, _d(wp, dev), _d(ws, dev), sync)
+    assert np.array_equal(_h(sync), np.zeros(4, dtype=np.int32))
+    assert np.array_equal(_h(scales).view(np.uint32), s_ref.view(np.uint32))
+    assert np.array_equal(_h(codes), c_ref)
+    got = _h(y)
+    assert np.array_equal(got.view(np.uint16), y_ref.view(np.uint16)), \
+        f"{(got.view(np.uint16) != y_ref.view(np.uint16)).sum()} outputs differ"
+
+
+def test_fused_decode_reuses_its_sync_words(dev):
+    # Consecutive calls on one sync buffer with different inputs (each a new
+    # decode step) are all exact, and the buffer is zero after each.
+    from oracle import rotate_quant_ref
+    M, K, N, h = 4, 4096, 2048, 4096
+    rng = np.random.default_rng(77)
+    wp = workloads.random_weight_bytes(rng, N, K)
+    ws = workloads.random_scales(rng, N)
+    wpd, wsd = _d(wp, dev), _d(ws, dev)
+    sync = dptq.new_sync(dev)
+    for step in range(4):
+        x = workloads.gauss_outliers(rng, M, K)
+        bits = 4 if step % 2 == 0 else 8
+        y, _, _ = dptq.qlinear_decode_fused(_d(x, dev), h, bits, wpd, wsd, sync)
+        c_ref, s_ref = rotate_quant_ref(x, h, bits)
+        y_ref = epilogue_ref(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
+        assert np.array_equal(_h(y).view(np.uint16), y_ref.view(np.uint16)), f"step {step}"
+        assert np.array_equal(_h(sync), np.zeros(4, dtype=np.int32)), f"step {step}"
