@@ -138,27 +138,42 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
                         int32_t bits, const uint8_t* w_packed, const float* w_scales,
                         int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream);
 
+/* Paths of dptq_qlinear_decode_fused. */
+typedef enum {
+  DPTQ_DECODE_AUTO = 0,          /* the one launch where it is the faster path */
+  DPTQ_DECODE_ONE_LAUNCH = 1,    /* rotation repeated in every workgroup */
+  DPTQ_DECODE_TWO_LAUNCHES = 2   /* dptq_rotate_quant, then the decode GEMM */
+} dptq_decode_mode;
+
 /*
- * dptq_qlinear_decode_fused - a decode-shape quantized linear in one launch:
- * dptq_rotate_quant followed by dptq_qlinear for M <= 16 tokens (Eq. 4, Eq. 2,
- * Section 2 Y = X W^T, Section 4.2 scales; the decode stage of Section 4.9),
- * with the same results bit for bit.  The rotation of the M rows overlaps
- * with the start of the weight stream instead of being a launch of its own.
+ * dptq_qlinear_decode_fused - a decode-shape quantized linear from the fp16
+ * activations: dptq_rotate_quant followed by dptq_qlinear for M <= 16 tokens
+ * (Eq. 4, Eq. 2, Section 2 Y = X W^T, Section 4.2 scales; the decode stage of
+ * Section 4.9), with the same results bit for bit on every path.
+ *
+ * DPTQ_DECODE_ONE_LAUNCH runs a single kernel in which every workgroup
+ * rotates and quantizes the M rows into on-chip memory while its first weight
+ * loads are in flight, then streams its weight slice against them: no second
+ * launch, and the GEMM never reads the codes back from HBM (workgroup 0 still
+ * stores them).  The rotation is repeated in every workgroup, so this path
+ * wins only for one or two rows of moderate K; DPTQ_DECODE_AUTO takes it for
+ * M <= 2, had_size a power of two <= 4096 (or 8192 with M = 1), K <= 12288
+ * and N <= 16384, and the two launches otherwise.
  *
  *   x, M, K, had_size, bits   as for dptq_rotate_quant; 1 <= M <= 16 (M = 0
- *            enqueues nothing), K a multiple of 128 and <= 32768
+ *            enqueues nothing), K a multiple of 128
  *   w_packed, w_scales, N, y  as for dptq_qlinear
  *   codes    device, the activation codes (dptq_rotate_quant layout), written
- *   a_scales device, float [M], written
- *   sync     device, int32 [4], 16-byte aligned, zero before the first call;
- *            the call leaves sync[0], sync[1] zero again.  sync[2] != 0 reports
- *            that a workgroup gave up waiting for the codes (not expected; the
- *            outputs of that call are then unspecified); clear it to reuse.
- *            Calls that share a sync buffer must not overlap in time.
+ *   a_scales device, float [M], written (16-byte aligned)
+ *   mode     a dptq_decode_mode
+ *
+ * DPTQ_DECODE_ONE_LAUNCH needs the rows on chip: M * (K * bits / 8 + 16)
+ * bytes of codes plus the fp32 staging of one row (17408 bytes per 4096
+ * elements of K, rounded up) at most 151 KiB, else DPTQ_ERR_UNSUPPORTED.
  */
 int dptq_qlinear_decode_fused(const void* x, int64_t M, int64_t K, int32_t had_size,
                               int32_t bits, const uint8_t* w_packed, const float* w_scales,
-                              int64_t N, void* y, void* codes, float* a_scales, int32_t* sync,
+                              int64_t N, void* y, void* codes, float* a_scales, int32_t mode,
                               void* stream);
 
 /*

@@ -17,7 +17,8 @@ import os
 __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qlinear_acc",
            "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
            "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
-           "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "new_sync",
+           "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "DECODE_AUTO", "DECODE_ONE_LAUNCH",
+           "DECODE_TWO_LAUNCHES",
            "qlinear_fp6_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
@@ -100,7 +101,7 @@ def lib():
         L.dptq_prepare_weights_signed.argtypes = [vp, i64, i64, i32, vp, vp, vp, vp]
         L.dptq_prepare_weights_signed.restype = ctypes.c_int
         L.dptq_qlinear_decode_fused.argtypes = [vp, i64, i64, i32, i32, vp, vp, i64, vp, vp, vp,
-                                                 vp, vp]
+                                                 i32, vp]
         L.dptq_qlinear_decode_fused.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
@@ -458,22 +459,19 @@ def qlinear_fp6_acc(a6, w6, M, K, N, acc=None):
     return acc
 
 
-def new_sync(device):
-    """A zeroed int32 [4] sync buffer for qlinear_decode_fused (reusable)."""
-    return _torch().zeros((4,), dtype=_torch().int32, device=device)
+DECODE_AUTO, DECODE_ONE_LAUNCH, DECODE_TWO_LAUNCHES = 0, 1, 2
 
 
-def qlinear_decode_fused(x, had_size, bits, w_packed, w_scales, sync, y=None, codes=None,
-                         scales=None):
-    """Decode-shape (M <= 16) rotate + quantize + GEMM in one launch.
-    Returns (y [M, N] fp16, codes, scales); sync from new_sync()."""
+def qlinear_decode_fused(x, had_size, bits, w_packed, w_scales, y=None, codes=None,
+                         scales=None, mode=DECODE_AUTO):
+    """Decode-shape (M <= 16) rotate + quantize + GEMM from fp16 x: one launch
+    or two (mode, DECODE_AUTO picks).  Returns (y [M, N] fp16, codes, scales)."""
     torch = _torch()
     _require(x, "x", torch.float16)
     M, K = x.shape
     N = w_packed.shape[0]
     _require(w_packed, "w_packed", torch.uint8, (N, K // 2))
     _require(w_scales, "w_scales", torch.float32, (N,))
-    _require(sync, "sync", torch.int32, (4,))
     cdt = torch.uint8 if bits == 4 else torch.int8
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=x.device)
@@ -486,5 +484,5 @@ def qlinear_decode_fused(x, had_size, bits, w_packed, w_scales, sync, y=None, co
     _require(scales, "scales", torch.float32, (M,))
     _check(lib().dptq_qlinear_decode_fused(_ptr(x), M, K, int(had_size), int(bits), _ptr(w_packed),
                                            _ptr(w_scales), N, _ptr(y), _ptr(codes), _ptr(scales),
-                                           _ptr(sync), _stream(x)), "dptq_qlinear_decode_fused")
+                                           int(mode), _stream(x)), "dptq_qlinear_decode_fused")
     return y, codes, scales

@@ -272,21 +272,24 @@ int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int
 
 int dptq_qlinear_decode_fused(const void* x, int64_t M, int64_t K, int32_t had_size,
                               int32_t bits, const uint8_t* w_packed, const float* w_scales,
-                              int64_t N, void* y, void* codes, float* a_scales, int32_t* sync,
+                              int64_t N, void* y, void* codes, float* a_scales, int32_t mode,
                               void* stream) {
   HadSplit hs{};
   int st = check_rotation_shape(M, K, had_size, &hs);
   if (st != DPTQ_OK) return st;
   st = check_gemm_shape(M, K, bits, N);
   if (st != DPTQ_OK) return st;
-  if (M > 16 || K > dptq::kMaxFusedK) return DPTQ_ERR_UNSUPPORTED;
+  if (mode < DPTQ_DECODE_AUTO || mode > DPTQ_DECODE_TWO_LAUNCHES) return DPTQ_ERR_INVALID_ARG;
+  if (M > 16) return DPTQ_ERR_UNSUPPORTED;
+  if (mode == DPTQ_DECODE_ONE_LAUNCH && dptq::decode_fused_lds(M, (int)K, hs, bits) > dptq::kFusedLdsMax)
+    return DPTQ_ERR_UNSUPPORTED;
   if (M == 0) return DPTQ_OK;
-  if (!x || !w_packed || !w_scales || !y || !codes || !a_scales || !sync) return DPTQ_ERR_INVALID_ARG;
+  if (!x || !w_packed || !w_scales || !y || !codes || !a_scales) return DPTQ_ERR_INVALID_ARG;
   if (!aligned16(x) || !aligned16(w_packed) || !aligned16(w_scales) || !aligned16(y) ||
-      !aligned16(codes) || !aligned4(a_scales) || !aligned16(sync))
+      !aligned16(codes) || !aligned16(a_scales))
     return DPTQ_ERR_INVALID_ARG;
   return from_hip(dptq::launch_decode_fused(x, M, (int)K, hs, bits, w_packed, w_scales, N, y, codes,
-                                            a_scales, sync, static_cast<hipStream_t>(stream)));
+                                            a_scales, mode, static_cast<hipStream_t>(stream)));
 }
 
 int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {

@@ -59,16 +59,23 @@ hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
                           const float* w_scales, int64_t N, void* y,
                           int32_t* out_acc, int kernel, hipStream_t stream);
 
-// Largest K of the fused decode kernel (its row staging plus the GEMM's
-// partial tiles fit in 160 KiB of LDS).
-constexpr int kMaxFusedK = 32768;
-// Decode-shape (M <= 16) rotate + quantize + GEMM + epilogue in one launch;
-// codes / a_scales receive the activation codes and scales; sync is the
-// caller's int32 [4] (zero before the first call, zero again after each call;
-// sync[2] != 0 reports a wait that gave up).
+// Dynamic LDS available to the fused decode kernel (160 KiB less its 8.1 KiB
+// of static arrays, rounded down).
+constexpr int64_t kFusedLdsMax = 151 * 1024;
+// Dynamic LDS the fused decode kernel needs for M rows of K at had split hs
+// and activation bits (with one row in flight; two when that also fits).
+int64_t decode_fused_lds(int64_t M, int K, HadSplit hs, int bits);
+// Decode-shape (M <= 16) rotate + quantize + GEMM + epilogue.  mode 1: one
+// launch, every workgroup rotating the M rows itself (requires
+// decode_fused_lds(M, K, hs, bits) <= kFusedLdsMax); mode 2: the
+// rotate+quantize kernel then the decode GEMM; mode 0: the one launch where
+// it is the faster (decode_one_launch_wins).  codes / a_scales receive the
+// activation codes and scales (both always written).
+constexpr int kDecodeAuto = 0, kDecodeOneLaunch = 1, kDecodeTwoLaunches = 2;
+bool decode_one_launch_wins(int64_t M, int K, HadSplit hs, int bits, int64_t N);
 hipError_t launch_decode_fused(const void* x, int64_t M, int K, HadSplit hs, int bits,
                                const uint8_t* w_packed, const float* w_scales, int64_t N, void* y,
-                               void* codes, float* a_scales, int32_t* sync, hipStream_t stream);
+                               void* codes, float* a_scales, int mode, hipStream_t stream);
 
 // Compute units of the current device (cached per device).
 int device_cus();

@@ -258,14 +258,24 @@ def test_fp6_entry_points_validation(L):
 
 
 def test_fused_decode_validation(L):
-    def call(M=4, K=4096, h=4096, bits=4, N=64, sync=FAKE, x=FAKE):
-        return L.dptq_qlinear_decode_fused(x, M, K, h, bits, FAKE, FAKE, N, FAKE, FAKE, FAKE,
-                                           sync, NULL)
+    def call(M=4, K=4096, h=4096, bits=4, N=64, x=FAKE, y=FAKE, codes=FAKE, scales=FAKE, mode=1):
+        return L.dptq_qlinear_decode_fused(x, M, K, h, bits, FAKE, FAKE, N, y, codes, scales, mode,
+                                           NULL)
     assert call(M=17) == UNSUPPORTED            # decode shapes only
-    assert call(K=36864, h=4096) == UNSUPPORTED # larger than the fused kernel's row staging
+    assert call(M=17, mode=2) == UNSUPPORTED
+    assert call(K=36864, h=4096) == UNSUPPORTED # one row's staging does not fit on chip
+    # 16 A8 rows of 14336 codes do not fit on chip for the one launch; the
+    # two launches take them (then the null y is the first error)
+    assert call(M=16, K=14336, h=28 * 512, bits=8) == UNSUPPORTED
+    assert call(M=16, K=14336, h=28 * 512, bits=8, mode=2, y=NULL) == INVALID
+    assert call(M=16, K=14336, h=28 * 512, bits=8, mode=0, y=NULL) == INVALID
+    assert call(mode=3) == INVALID
+    assert call(mode=-1) == INVALID
     assert call(bits=6) == INVALID
-    assert call(sync=NULL) == INVALID
-    assert call(sync=MISALIGNED) == INVALID
+    assert call(y=NULL) == INVALID
+    assert call(codes=NULL) == INVALID
+    assert call(scales=NULL) == INVALID
+    assert call(codes=MISALIGNED) == INVALID
     assert call(N=24) == UNSUPPORTED
     assert call(h=3) == INVALID
     assert call(M=0, x=NULL) == OK

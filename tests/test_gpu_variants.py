@@ -106,26 +106,32 @@ def test_signed_layer_end_to_end(dev, bits):
 
 FUSED_CASES = [
     # (M, K, N, h, bits): LLaMA decode shapes (7B QKV, 8B down with h = 28 x 512,
-    # 7B down with 43 blocks of 256, 70B QKV at h = 8192), the tiny workload,
-    # and grids smaller than M (a workgroup produces several rows)
+    # 7B down with 43 blocks of 256, 70B QKV at h = 8192, 70B down at
+    # h = 28 x 1024 with N cut to keep the oracle quick), the tiny workload,
+    # odd M (the second row slot idle), a K that is not a multiple of 4096,
+    # M = 16 with one row in flight, h = 28 (no butterflies), h = 2^14 (two
+    # passes across segments)
     (1, 4096, 12288, 4096, 4), (4, 14336, 4096, 28 * 512, 4), (16, 256, 512, 256, 8),
     (8, 11008, 4096, 256, 4), (8, 8192, 1024, 8192, 8), (3, 512, 32, 512, 4),
-    (16, 1024, 16, 1024, 8), (16, 4096, 12288, 4096, 8),
+    (16, 1024, 16, 1024, 8), (16, 4096, 12288, 4096, 8), (16, 11008, 4096, 256, 4),
+    (5, 6144, 256, 2048, 8), (2, 7168, 512, 28 * 256, 8), (1, 28672, 64, 28 * 1024, 4),
+    (3, 896, 32, 28, 8), (2, 16384, 64, 16384, 8), (1, 14336, 4096, 28 * 512, 8),
 ]
+# Shapes whose rows do not fit on chip: the two-launch path only.
+TWO_LAUNCH_ONLY = [(16, 14336, 4096, 28 * 512, 8), (8, 28672, 256, 28 * 1024, 4),
+                   (16, 14336, 512, 28 * 512, 4)]
 
 
-@pytest.mark.parametrize("M,K,N,h,bits", FUSED_CASES)
-def test_fused_decode_matches_oracle(dev, M, K, N, h, bits):
-    from oracle import rotate_quant_ref, prepare_weights_ref
+def _fused_case(dev, M, K, N, h, bits, mode):
+    from oracle import rotate_quant_ref
     rng = np.random.default_rng(M * 31 + K + N + bits)
     x = workloads.student_t(rng, M, K) if h % 28 == 0 else workloads.gauss_outliers(rng, M, K)
     wp = workloads.random_weight_bytes(rng, N, K)
     ws = workloads.random_scales(rng, N)
     c_ref, s_ref = rotate_quant_ref(x, h, bits)
     y_ref = epilogue_ref(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
-    sync = dptq.new_sync(dev)
-    y, codes, scales = dptq.qlinear_decode_fused(_d(x, dev), h, bits, _d(wp, dev), _d(ws, dev), sync)
-    assert np.array_equal(_h(sync), np.zeros(4, dtype=np.int32))
+    y, codes, scales = dptq.qlinear_decode_fused(_d(x, dev), h, bits, _d(wp, dev), _d(ws, dev),
+                                                 mode=mode)
     assert np.array_equal(_h(scales).view(np.uint32), s_ref.view(np.uint32))
     assert np.array_equal(_h(codes), c_ref)
     got = _h(y)
@@ -133,21 +139,45 @@ def test_fused_decode_matches_oracle(dev, M, K, N, h, bits):
         f"{(got.view(np.uint16) != y_ref.view(np.uint16)).sum()} outputs differ"
 
 
-def test_fused_decode_reuses_its_sync_words(dev):
-    # Consecutive calls on one sync buffer with different inputs (each a new
-    # decode step) are all exact, and the buffer is zero after each.
+@pytest.mark.parametrize("M,K,N,h,bits", FUSED_CASES)
+def test_fused_decode_one_launch_matches_oracle(dev, M, K, N, h, bits):
+    _fused_case(dev, M, K, N, h, bits, dptq.DECODE_ONE_LAUNCH)
+
+
+@pytest.mark.parametrize("M,K,N,h,bits", FUSED_CASES[:4] + TWO_LAUNCH_ONLY)
+def test_fused_decode_two_launches_matches_oracle(dev, M, K, N, h, bits):
+    _fused_case(dev, M, K, N, h, bits, dptq.DECODE_TWO_LAUNCHES)
+
+
+@pytest.mark.parametrize("M,K,N,h,bits", [(1, 4096, 4096, 4096, 4), (2, 8192, 512, 8192, 8),
+                                          (16, 14336, 512, 28 * 512, 8)])
+def test_fused_decode_auto_matches_oracle(dev, M, K, N, h, bits):
+    _fused_case(dev, M, K, N, h, bits, dptq.DECODE_AUTO)
+
+
+def test_fused_decode_one_launch_rejects_rows_that_do_not_fit(dev):
+    x = torch.zeros((16, 14336), dtype=torch.float16, device=dev)
+    wp = torch.zeros((64, 7168), dtype=torch.uint8, device=dev)
+    ws = torch.ones((64,), dtype=torch.float32, device=dev)
+    with pytest.raises(dptq.DptqError):
+        dptq.qlinear_decode_fused(x, 28 * 512, 8, wp, ws, mode=dptq.DECODE_ONE_LAUNCH)
+
+
+def test_fused_decode_consecutive_calls(dev):
+    # Consecutive decode steps with different inputs, M and bits on the same
+    # weights are all exact on the one-launch path.
     from oracle import rotate_quant_ref
-    M, K, N, h = 4, 4096, 2048, 4096
+    K, N, h = 4096, 2048, 4096
     rng = np.random.default_rng(77)
     wp = workloads.random_weight_bytes(rng, N, K)
     ws = workloads.random_scales(rng, N)
     wpd, wsd = _d(wp, dev), _d(ws, dev)
-    sync = dptq.new_sync(dev)
-    for step in range(4):
+    for step, M in enumerate([4, 1, 16, 7]):
         x = workloads.gauss_outliers(rng, M, K)
         bits = 4 if step % 2 == 0 else 8
-        y, _, _ = dptq.qlinear_decode_fused(_d(x, dev), h, bits, wpd, wsd, sync)
+        y, _, scales = dptq.qlinear_decode_fused(_d(x, dev), h, bits, wpd, wsd,
+                                                 mode=dptq.DECODE_ONE_LAUNCH)
         c_ref, s_ref = rotate_quant_ref(x, h, bits)
         y_ref = epilogue_ref(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
         assert np.array_equal(_h(y).view(np.uint16), y_ref.view(np.uint16)), f"step {step}"
-        assert np.array_equal(_h(sync), np.zeros(4, dtype=np.int32)), f"step {step}"
+        assert np.array_equal(_h(scales).view(np.uint32), s_ref.view(np.uint32))
