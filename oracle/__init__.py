@@ -25,6 +25,8 @@ Modules
             (Section 4.2, Eq. 1-2).
   variants  the randomized-sign (QuaRot-style) rotation of Section 4.2 and
             its weight absorption (Eq. 4-5).
+  range_quant  the range-based quantizer of Eq. 1 with an integer zero point,
+            and the zero-point correction of the integer GEMM.
 """
 
 from .hadamard import (sylvester, paley28, hadamard, split_had_size,
@@ -38,6 +40,9 @@ from .residual import (jump_ratio_tokens_ref, inverse_rotate_f64, reconstructed_
 from .kv import kv_quant_ref, kv_dequant_ref, pack_u4, unpack_u4
 from .variants import (signs_from_bits, apply_signs, rotate_quant_signed_ref,
                        prepare_weights_signed_ref)
+from .range_quant import (range_levels, quantize_rows_range, rotate_quant_range_ref,
+                          dequant_rows_range, weight_sums_ref, zero_point_acc_ref,
+                          qlinear_range_ref)
 
 __all__ = [
     "sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows",
@@ -49,4 +54,6 @@ __all__ = [
     "hist_snr_tokens_ref", "residual_dynamics_ref", "select_sensitive_layers_ref",
     "kv_quant_ref", "kv_dequant_ref", "pack_u4", "unpack_u4",
     "signs_from_bits", "apply_signs", "rotate_quant_signed_ref", "prepare_weights_signed_ref",
+    "range_levels", "quantize_rows_range", "rotate_quant_range_ref", "dequant_rows_range",
+    "weight_sums_ref", "zero_point_acc_ref", "qlinear_range_ref",
 ]
