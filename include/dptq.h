@@ -177,6 +177,63 @@ int dptq_qlinear_decode_fused(const void* x, int64_t M, int64_t K, int32_t had_s
                               void* stream);
 
 /*
+ * dptq_rotate_quant_range - dptq_rotate_quant with the range-based quantizer
+ * of Eq. 1 and an integer zero point instead of the symmetric one (Eq. 4 and
+ * Eq. 1-2; Algorithm 1 lists zero points among the quantizer parameters).
+ * Per token row y of x B_h (rotated exactly as dptq_rotate_quant rotates):
+ *
+ *   mx = max(max y, 0), mn = min(min y, 0)    (the range covers 0: zero is a level)
+ *   s  = fl32(fl32(mx - mn) / (2^bits - 1))   one IEEE division per row
+ *   z  = clamp(RNE(fl32(-mn / s)), 0, 2^bits - 1)
+ *   q  = clamp(RNE(fl32(y / s)) + z, 0, 2^bits - 1),   Q(y) = s (q - z)
+ *
+ * and the stored code is q - 2^(bits-1), packed as dptq_rotate_quant packs
+ * (4-bit two's complement nibbles, or int8).  A row of zeros gets s = 0,
+ * z = 0 and q = 0.
+ *
+ *   x, M, K, had_size, bits   as for dptq_rotate_quant, K a multiple of 128
+ *                             (else DPTQ_ERR_UNSUPPORTED)
+ *   codes     device, output, dptq_rotate_quant's layout
+ *   a_scales  device, float [M] output (s)
+ *   a_zeros   device, int32 [M] output (z)
+ */
+int dptq_rotate_quant_range(const void* x, int64_t M, int64_t K, int32_t had_size, int32_t bits,
+                            void* codes, float* a_scales, int32_t* a_zeros, void* stream);
+
+/*
+ * dptq_weight_sums - w_sums[n] = sum over k of weight row n's 4-bit codes (the
+ * per-channel term of the zero-point correction in dptq_qlinear_range).
+ *
+ *   w_packed  device, uint8 [N, K/2] (dptq_prepare_weights layout), 16-byte aligned
+ *   N, K      N >= 0, K a multiple of 32 (else DPTQ_ERR_UNSUPPORTED)
+ *   w_sums    device, int32 [N] output
+ */
+int dptq_weight_sums(const uint8_t* w_packed, int64_t N, int64_t K, int32_t* w_sums, void* stream);
+
+/*
+ * dptq_qlinear_range - the quantized linear on range-quantized activations
+ * (Section 2 Y = X W^T with Q(y) = s (q - z)): the exact integer GEMM of the
+ * stored codes, corrected by the zero point,
+ *
+ *   acc'[m, n] = acc[m, n] + (2^(bits-1) - a_zeros[m]) w_sums[n]
+ *             = sum_k (q[m, k] - a_zeros[m]) w[n, k]            (exact int32)
+ *   y[m, n]    = fl16(fl32(fl32(fl32(acc'[m, n]) * a_scales[m]) * w_scales[n]))
+ *
+ * Two launches: dptq_qlinear_acc's GEMM into acc, then the correction and
+ * epilogue.
+ *
+ *   codes, a_scales, a_zeros  dptq_rotate_quant_range's outputs for M rows
+ *   M, K, bits, w_packed, w_scales, N   as for dptq_qlinear
+ *   w_sums    device, int32 [N] (dptq_weight_sums), 16-byte aligned
+ *   acc       device, int32 [M, N] workspace, 16-byte aligned; holds the
+ *             uncorrected accumulator afterwards
+ *   y         device, fp16 [M, N] output, 16-byte aligned
+ */
+int dptq_qlinear_range(const void* codes, const float* a_scales, const int32_t* a_zeros, int64_t M,
+                       int64_t K, int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                       const int32_t* w_sums, int64_t N, int32_t* acc, void* y, void* stream);
+
+/*
  * dptq_residual_dynamics - residual-dynamics calibration statistics of one
  * layer (Section 3.1 Eq. 8-11; quantization in the rotated space, Section 3.2
  * Eq. 14-16).  For every token row t of the residual state x entering the

@@ -18,7 +18,7 @@ __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qline
            "layer_policy", "prepare_weights", "residual_dynamics", "select_layers",
            "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
            "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "DECODE_AUTO", "DECODE_ONE_LAUNCH",
-           "DECODE_TWO_LAUNCHES",
+           "DECODE_TWO_LAUNCHES", "rotate_quant_range", "weight_sums", "qlinear_range",
            "qlinear_fp6_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
@@ -35,7 +35,8 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_layer_policy", "dptq_prepare_weights",
                       "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_rotate_quant_fp6",
                       "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed",
-                      "dptq_qlinear_decode_fused")
+                      "dptq_qlinear_decode_fused", "dptq_rotate_quant_range",
+                      "dptq_weight_sums", "dptq_qlinear_range")
 
 # Code layouts of dptq_rotate_quant_ex.
 LAYOUT_PACKED, LAYOUT_FP6 = 0, 1
@@ -103,6 +104,12 @@ def lib():
         L.dptq_qlinear_decode_fused.argtypes = [vp, i64, i64, i32, i32, vp, vp, i64, vp, vp, vp,
                                                  i32, vp]
         L.dptq_qlinear_decode_fused.restype = ctypes.c_int
+        L.dptq_rotate_quant_range.argtypes = [vp, i64, i64, i32, i32, vp, vp, vp, vp]
+        L.dptq_rotate_quant_range.restype = ctypes.c_int
+        L.dptq_weight_sums.argtypes = [vp, i64, i64, vp, vp]
+        L.dptq_weight_sums.restype = ctypes.c_int
+        L.dptq_qlinear_range.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp, i64, vp, vp, vp]
+        L.dptq_qlinear_range.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
         _lib = L
@@ -486,3 +493,63 @@ def qlinear_decode_fused(x, had_size, bits, w_packed, w_scales, y=None, codes=No
                                            _ptr(w_scales), N, _ptr(y), _ptr(codes), _ptr(scales),
                                            int(mode), _stream(x)), "dptq_qlinear_decode_fused")
     return y, codes, scales
+
+
+def rotate_quant_range(x, had_size, bits, codes=None, scales=None, zeros=None):
+    """Rotation + per-token range quantization with an integer zero point.
+    Returns (codes, scales fp32 [M], zeros int32 [M])."""
+    torch = _torch()
+    _require(x, "x", torch.float16)
+    M, K = x.shape
+    cdt = torch.uint8 if bits == 4 else torch.int8
+    if codes is None:
+        codes = torch.empty(code_shape(M, K, bits), dtype=cdt, device=x.device)
+    if scales is None:
+        scales = torch.empty((M,), dtype=torch.float32, device=x.device)
+    if zeros is None:
+        zeros = torch.empty((M,), dtype=torch.int32, device=x.device)
+    _require(codes, "codes", cdt, code_shape(M, K, bits))
+    _require(scales, "scales", torch.float32, (M,))
+    _require(zeros, "zeros", torch.int32, (M,))
+    _check(lib().dptq_rotate_quant_range(_ptr(x), M, K, int(had_size), int(bits), _ptr(codes),
+                                         _ptr(scales), _ptr(zeros), _stream(x)),
+           "dptq_rotate_quant_range")
+    return codes, scales, zeros
+
+
+def weight_sums(w_packed, out=None):
+    """int32 [N]: the sum of each packed 4-bit weight row's codes."""
+    torch = _torch()
+    _require(w_packed, "w_packed", torch.uint8)
+    N, K2 = w_packed.shape
+    if out is None:
+        out = torch.empty((N,), dtype=torch.int32, device=w_packed.device)
+    _require(out, "out", torch.int32, (N,))
+    _check(lib().dptq_weight_sums(_ptr(w_packed), N, 2 * K2, _ptr(out), _stream(w_packed)),
+           "dptq_weight_sums")
+    return out
+
+
+def qlinear_range(codes, scales, zeros, bits, w_packed, w_scales, w_sums, y=None, acc=None):
+    """Quantized linear on range-quantized activations (zero-point corrected).
+    Returns y [M, N] fp16; acc (int32 [M, N] workspace) holds the raw accumulator."""
+    torch = _torch()
+    M = scales.shape[0]
+    N, K2 = w_packed.shape
+    K = 2 * K2
+    _require(codes, "codes", torch.uint8 if bits == 4 else torch.int8, code_shape(M, K, bits))
+    _require(scales, "scales", torch.float32, (M,))
+    _require(zeros, "zeros", torch.int32, (M,))
+    _require(w_packed, "w_packed", torch.uint8, (N, K2))
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    _require(w_sums, "w_sums", torch.int32, (N,))
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=codes.device)
+    _require(y, "y", torch.float16, (M, N))
+    _require(acc, "acc", torch.int32, (M, N))
+    _check(lib().dptq_qlinear_range(_ptr(codes), _ptr(scales), _ptr(zeros), M, K, int(bits),
+                                    _ptr(w_packed), _ptr(w_scales), _ptr(w_sums), N, _ptr(acc),
+                                    _ptr(y), _stream(codes)), "dptq_qlinear_range")
+    return y

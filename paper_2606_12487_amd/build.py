@@ -19,7 +19,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libdptq.so")
 
-SOURCES = ["dptq_api.hip", "rotate_quant.hip", "qgemm.hip", "qgemm_fp6.hip", "decode_fused.hip", "kv_quant.hip"]
+SOURCES = ["dptq_api.hip", "rotate_quant.hip", "qgemm.hip", "qgemm_fp6.hip", "decode_fused.hip", "kv_quant.hip",
+           "range_quant.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -56,20 +56,6 @@ __device__ __forceinline__ __half f_dequant(int acc, float as, float ws) {
   return __float2half_rn(t2);
 }
 
-// u where ok, else zero (component-wise selects).
-__device__ __forceinline__ uint4 f_keep(bool ok, uint4 u) {
-  return make_uint4(ok ? u.x : 0u, ok ? u.y : 0u, ok ? u.z : 0u, ok ? u.w : 0u);
-}
-
-__device__ __forceinline__ void f_widen8(uint4 u, float* d) {
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    d[2 * k] = __half2float(__ushort_as_half((unsigned short)(w[k] & 0xFFFFu)));
-    d[2 * k + 1] = __half2float(__ushort_as_half((unsigned short)(w[k] >> 16)));
-  }
-}
-
 // Codes of 8 consecutive elements stored at element e of a row: to the LDS
 // row, and to the global row when there is one.
 template <int BITS>
@@ -85,19 +71,11 @@ __device__ __forceinline__ void f_store8(const uint32_t* bt, int e, uint8_t* cl,
   }
 }
 
-// Float offset of element i of a row staged as 4096-element segments.
-__device__ __forceinline__ int f_sidx(int i) { return (i >> 12) * kSegFloats + seg_off(i & (kSeg - 1)); }
-
-// h = F * 2^J (F = 28 when F28, else 1; JP = min(J, 12)): rows m0 and, with two rows in
-// flight (rif = 2), m0 + 1.  Threads 256 * half + r (r < 256) hold 16
-// elements of a 4096-element segment of row m0 + half in each of three
-// register phases covering index bits 0-3, 4-7 and 8-11, in that order; bits
-// 12 and up pair whole segments, one LDS pass per bit; for F = 28 a last pass
-// gives each thread whole columns of the dense 28-point stage.  K is a
-// multiple of 128, so a thread's 16 elements are all in the row or all past
-// it; past the row end the segment is zero (whole Hadamard blocks of zeros).
-// With use_pre, p0 and p1 hold this thread's first 16 elements of segment 0,
-// loaded by the caller (any values where they lie past the row end).
+// Rotate + quantize rows m0 and, with two rows in flight (rif = 2), m0 + 1:
+// threads 256 * half + r (r < 256) rotate row m0 + half in its own staging
+// (rotate_row_segments), then quantize it into the LDS code rows (and the
+// caller's buffers when given).  p0, p1 with use_pre: this thread's first 16
+// elements of segment 0, loaded by the caller.
 template <int BITS, int JP, bool F28>
 __device__ __forceinline__ void rows_fast(const __half* __restrict__ x, int M, int K, int J,
                                           int m0, int rif, bool use_pre, uint4 p0, uint4 p1,
@@ -110,115 +88,9 @@ __device__ __forceinline__ void rows_fast(const __half* __restrict__ x, int M, i
   const int nseg = (K + kSeg - 1) / kSeg;
   float* rh = rot + half * nseg * kSegFloats;
   const int b1 = seg_off(16 * r);
-  const int b2 = seg_off(256 * (r >> 4) + (r & 15));
-  const int b3 = seg_off(r);
   const __half* xr = x + (size_t)m * K;
-  float tmax = 0.0f;
-  if (act) {
-    for (int sg = 0; sg < nseg; ++sg) {
-      const int e = sg * kSeg + 16 * r;
-      float v[16];
-      if (use_pre && sg == 0) {
-        f_widen8(f_keep(e < K, p0), v);
-        f_widen8(f_keep(e < K, p1), v + 8);
-      } else {
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2)
-          f_widen8(e < K ? *reinterpret_cast<const uint4*>(xr + e + 8 * h2) : make_uint4(0, 0, 0, 0),
-                   v + 8 * h2);
-      }
-      stages16<0, (JP < 4 ? JP : 4)>(v);
-      if (JP <= 4) tmax = absmax16(v, tmax);
-      float* sl = rh + sg * kSegFloats + b1;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(sl + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
-    }
-  }
-  if constexpr (JP > 4) {
-    __syncthreads();
-    if (act) {
-      for (int sg = 0; sg < nseg; ++sg) {
-        if (sg * kSeg >= K) continue;
-        float* sl = rh + sg * kSegFloats + b2;
-        float v[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) v[q] = sl[16 * q + 4 * (q >> 2)];
-        stages16<0, (JP < 8 ? JP : 8) - 4>(v);
-        if (JP <= 8) tmax = absmax16(v, tmax);
-#pragma unroll
-        for (int q = 0; q < 16; ++q) sl[16 * q + 4 * (q >> 2)] = v[q];
-      }
-    }
-  }
-  if constexpr (JP > 8) {
-    __syncthreads();
-    if (act) {
-      for (int sg = 0; sg < nseg; ++sg) {
-        if (sg * kSeg >= K) continue;
-        float* sl = rh + sg * kSegFloats + b3;
-        float v[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) v[q] = sl[272 * q];
-        stages16<0, JP - 8>(v);
-        tmax = absmax16(v, tmax);
-#pragma unroll
-        for (int q = 0; q < 16; ++q) sl[272 * q] = v[q];
-      }
-    }
-  }
-  if (F28 || (JP == 12 && J > 12)) {
-    // The row maximum is taken in the last pass instead.
-    tmax = 0.0f;
-    for (int b = 12; JP == 12 && b < J; ++b) {
-      // Bit b: segments s and s + 2^(b - 12), s with that bit clear.
-      __syncthreads();
-      if (act) {
-        const int S = 1 << (b - 12);
-        const bool last_pass = b == J - 1 && !F28;
-        for (int sg = 0; sg < nseg; ++sg) {
-          if (sg & S) continue;
-          float* lo = rh + sg * kSegFloats + b1;
-          float* hi = lo + S * kSegFloats;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float4 a = *reinterpret_cast<const float4*>(lo + 4 * q);
-            const float4 c = *reinterpret_cast<const float4*>(hi + 4 * q);
-            const float4 s4 = make_float4(a.x + c.x, a.y + c.y, a.z + c.z, a.w + c.w);
-            const float4 d4 = make_float4(a.x - c.x, a.y - c.y, a.z - c.z, a.w - c.w);
-            *reinterpret_cast<float4*>(lo + 4 * q) = s4;
-            *reinterpret_cast<float4*>(hi + 4 * q) = d4;
-            if (last_pass) {
-              tmax = fmaxf(fmaxf(fmaxf(fabsf(s4.x), fabsf(s4.y)), fmaxf(fabsf(s4.z), fabsf(s4.w))), tmax);
-              tmax = fmaxf(fmaxf(fmaxf(fabsf(d4.x), fabsf(d4.y)), fmaxf(fabsf(d4.z), fabsf(d4.w))), tmax);
-            }
-          }
-        }
-      }
-    }
-    if constexpr (F28) {
-      // y[b p + c] = sum over a = 0..27, in order, of H28[a][b] z[a p + c],
-      // one column (block, c) per thread at a time.
-      __syncthreads();
-      if (act) {
-        const int p = 1 << J;
-        for (int col = r; col < K / 28; col += 256) {
-          const int base = (col >> J) * 28 * p + (col & (p - 1));
-          float z[28];
-#pragma unroll
-          for (int a = 0; a < 28; ++a) z[a] = rh[f_sidx(base + a * p)];
-#pragma unroll
-          for (int bb = 0; bb < 28; ++bb) {
-            float acc = kH28.e[0][bb] > 0 ? z[0] : -z[0];
-#pragma unroll
-            for (int a = 1; a < 28; ++a) acc = kH28.e[a][bb] > 0 ? acc + z[a] : acc - z[a];
-            rh[f_sidx(base + bb * p)] = acc;
-            tmax = fmaxf(tmax, fabsf(acc));
-          }
-        }
-      }
-    }
-  }
+  float tmax = 0.0f, unused = 0.0f;
+  rotate_row_segments<JP, F28, false>(xr, K, J, act, r, use_pre, p0, p1, rh, tmax, unused);
   // Row maximum: waves 0-3 hold row m0, waves 4-7 row m0 + 1.
   tmax = wave_max_nonneg(tmax);
   if ((t & 63) == 0) red[t >> 6] = tmax;
@@ -307,7 +179,7 @@ qdecode_fused(const __half* __restrict__ x, int M, int K, int J, int rif,
   for (int k = 0; k < kFBatch; ++k) {
     const int ck = c_begin + k;
     const uint4 u = *reinterpret_cast<const uint4*>(wp + (size_t)min(ck, last) * 64);
-    wv[k] = f_keep(ck < c_end, u);
+    wv[k] = keep_or_zero(ck < c_end, u);
   }
   __builtin_amdgcn_sched_barrier(0);     // ... then the weights, then the rotation
 
@@ -323,7 +195,7 @@ qdecode_fused(const __half* __restrict__ x, int M, int K, int J, int rif,
       for (int k = 0; k < kFBatch; ++k) {
         const int ck = c + k;
         const uint4 u = *reinterpret_cast<const uint4*>(wp + (size_t)min(ck, last) * 64);
-        wv[k] = f_keep(ck < c_end, u);
+        wv[k] = keep_or_zero(ck < c_end, u);
       }
     }
     // The codes come from LDS chunk by chunk (short latency, few registers).
@@ -334,12 +206,12 @@ qdecode_fused(const __half* __restrict__ x, int M, int K, int J, int rif,
       const int cc = min(ck, c_end - 1);   // c < c_end: a chunk of this wavefront
       v4i_t b0, b1;
       if (BITS == 4) {
-        const uint4 u = f_keep(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 64));
+        const uint4 u = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 64));
         b0 = f_op_nibbles(u.x, u.y);
         b1 = f_op_nibbles(u.z, u.w);
       } else {
-        const uint4 u = f_keep(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128));
-        const uint4 u2 = f_keep(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128 + 16));
+        const uint4 u = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128));
+        const uint4 u2 = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128 + 16));
         b0 = f_op_bytes(u.x, u.y, u.z, u.w);
         b1 = f_op_bytes(u2.x, u2.y, u2.z, u2.w);
       }

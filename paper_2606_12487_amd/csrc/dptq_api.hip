@@ -292,6 +292,49 @@ int dptq_qlinear_decode_fused(const void* x, int64_t M, int64_t K, int32_t had_s
                                             a_scales, mode, static_cast<hipStream_t>(stream)));
 }
 
+int dptq_rotate_quant_range(const void* x, int64_t M, int64_t K, int32_t had_size, int32_t bits,
+                            void* codes, float* a_scales, int32_t* a_zeros, void* stream) {
+  HadSplit hs{};
+  int st = check_rotation_shape(M, K, had_size, &hs);
+  if (st != DPTQ_OK) return st;
+  if (bits != 4 && bits != 8) return DPTQ_ERR_INVALID_ARG;
+  if (K % 128 != 0) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!x || !codes || !a_scales || !a_zeros) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(codes) || !aligned4(a_scales) || !aligned4(a_zeros))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_rotate_quant_range(x, M, (int)K, hs, bits, codes, a_scales, a_zeros,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
+int dptq_weight_sums(const uint8_t* w_packed, int64_t N, int64_t K, int32_t* w_sums, void* stream) {
+  if (N < 0 || K < 1) return DPTQ_ERR_INVALID_ARG;
+  if (K % 32 != 0 || K > DPTQ_MAX_K || N > 0x7FFFFFF0) return DPTQ_ERR_UNSUPPORTED;
+  if (N == 0) return DPTQ_OK;
+  if (!w_packed || !w_sums || !aligned16(w_packed) || !aligned4(w_sums)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_weight_sums(w_packed, N, (int)K, w_sums,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int dptq_qlinear_range(const void* codes, const float* a_scales, const int32_t* a_zeros, int64_t M,
+                       int64_t K, int32_t bits, const uint8_t* w_packed, const float* w_scales,
+                       const int32_t* w_sums, int64_t N, int32_t* acc, void* y, void* stream) {
+  int st = check_gemm_shape(M, K, bits, N);
+  if (st != DPTQ_OK) return st;
+  if (M == 0) return DPTQ_OK;
+  if (!codes || !a_scales || !a_zeros || !w_packed || !w_scales || !w_sums || !acc || !y)
+    return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned4(a_scales) || !aligned4(a_zeros) || !aligned16(w_packed) ||
+      !aligned16(w_scales) || !aligned16(w_sums) || !aligned16(acc) || !aligned16(y))
+    return DPTQ_ERR_INVALID_ARG;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = dptq::launch_qlinear(codes, nullptr, M, (int)K, bits, w_packed, nullptr, N, nullptr,
+                                      acc, dptq::kGemmAuto, s);
+  if (e != hipSuccess) return from_hip(e);
+  return from_hip(dptq::launch_range_epilogue(acc, a_scales, a_zeros, bits, w_sums, w_scales, M, N,
+                                               y, s));
+}
+
 int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {
   if (num_layers < 1 || !bits_out) return DPTQ_ERR_INVALID_ARG;
   for (int32_t l = 0; l < num_layers; ++l) {

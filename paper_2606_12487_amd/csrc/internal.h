@@ -77,6 +77,19 @@ hipError_t launch_decode_fused(const void* x, int64_t M, int K, HadSplit hs, int
                                const uint8_t* w_packed, const float* w_scales, int64_t N, void* y,
                                void* codes, float* a_scales, int mode, hipStream_t stream);
 
+// Range-based quantizer with an integer zero point (rows of K % 128 == 0):
+// codes (q - 2^(b-1), the symmetric path's packing), scales, zeros [M].
+hipError_t launch_rotate_quant_range(const void* x, int64_t M, int K, HadSplit hs, int bits,
+                                     void* codes, float* scales, int32_t* zeros,
+                                     hipStream_t stream);
+// sums[n] = sum of weight row n's 4-bit codes (K % 32 == 0).
+hipError_t launch_weight_sums(const uint8_t* w_packed, int64_t N, int K, int32_t* sums,
+                              hipStream_t stream);
+// y = epilogue(acc + (2^(b-1) - zeros[m]) * w_sums[n]) from the raw accumulator.
+hipError_t launch_range_epilogue(const int32_t* acc, const float* a_scales, const int32_t* a_zeros,
+                                 int bits, const int32_t* w_sums, const float* w_scales, int64_t M,
+                                 int64_t N, void* y, hipStream_t stream);
+
 // Compute units of the current device (cached per device).
 int device_cus();
 

@@ -1,9 +1,10 @@
-// Device helpers of the quantizer shared by the rotate+quantize kernels and
-// the fused decode kernel: the H28 table, the rounding of y / s to a code, and
-// code packing.
+// Device helpers of the quantizer shared by the rotate+quantize kernels, the
+// range quantizer and the fused decode kernel: the H28 table, the rounding of
+// y / s to a code, code packing, and the segmented row rotation.
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
 #include <stdint.h>
 
 namespace dptq {
@@ -108,6 +109,177 @@ __device__ __forceinline__ float wave_max_nonneg(float m) {
   const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
   const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
   return __int_as_float(max(max(r0, r1), max(r2, r3)));
+}
+
+// ---------------------------------------------------------------------------
+// One row rotated by 256 threads (r = 0..255) in 4096-element LDS segments,
+// for h = F * 2^J with F = 28 when F28, else 1, and JP = min(J, 12).  Each
+// thread holds 16 elements of a segment in each of three register phases
+// covering index bits 0-3, 4-7 and 8-11, in that order; bits 12 and up pair
+// whole segments, one LDS pass per bit; for F = 28 a last pass gives each
+// thread whole columns of the dense 28-point stage, summed in order over the
+// slow index.  K is a multiple of 128, so a thread's 16 elements are all in
+// the row or all past it; past the row end the segment is zero (whole
+// Hadamard blocks of zeros).  The rotated row is left in rh (element i at
+// seg_index(i)).  Every thread of the workgroup calls this (it holds
+// barriers); act = false threads only join them.  With use_pre, p0 and p1 are
+// this thread's first 16 elements of segment 0, loaded by the caller.
+//
+// Row maxima, each starting at 0: RANGE = false keeps the absolute maximum
+// in ma; RANGE = true keeps max(0, max v) in ma and max(0, max -v) in mb.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int seg_index(int i) { return (i >> 12) * kSegFloats + seg_off(i & (kSeg - 1)); }
+
+// u where ok, else zero (component-wise selects).
+__device__ __forceinline__ uint4 keep_or_zero(bool ok, uint4 u) {
+  return make_uint4(ok ? u.x : 0u, ok ? u.y : 0u, ok ? u.z : 0u, ok ? u.w : 0u);
+}
+
+// Eight fp16 values (one 16-byte load) widened to fp32.
+__device__ __forceinline__ void widen8(uint4 u, float* d) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    d[2 * k] = __half2float(__ushort_as_half((unsigned short)(w[k] & 0xFFFFu)));
+    d[2 * k + 1] = __half2float(__ushort_as_half((unsigned short)(w[k] >> 16)));
+  }
+}
+
+template <bool RANGE>
+__device__ __forceinline__ void row_max1(float v, float& ma, float& mb) {
+  if constexpr (RANGE) {
+    ma = fmaxf(ma, v);
+    mb = fmaxf(mb, -v);
+  } else {
+    ma = fmaxf(ma, fabsf(v));
+  }
+}
+
+template <bool RANGE>
+__device__ __forceinline__ void row_max16(const float* v, float& ma, float& mb) {
+  if constexpr (RANGE) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) row_max1<true>(v[q], ma, mb);
+  } else {
+    ma = absmax16(v, ma);
+  }
+}
+
+template <int JP, bool F28, bool RANGE>
+__device__ __forceinline__ void rotate_row_segments(const __half* __restrict__ xr, int K, int J,
+                                                    bool act, int r, bool use_pre, uint4 p0,
+                                                    uint4 p1, float* rh, float& ma, float& mb) {
+  const int nseg = (K + kSeg - 1) / kSeg;
+  const int b1 = seg_off(16 * r);
+  const int b2 = seg_off(256 * (r >> 4) + (r & 15));
+  const int b3 = seg_off(r);
+  if (act) {
+    for (int sg = 0; sg < nseg; ++sg) {
+      const int e = sg * kSeg + 16 * r;
+      float v[16];
+      if (use_pre && sg == 0) {
+        widen8(keep_or_zero(e < K, p0), v);
+        widen8(keep_or_zero(e < K, p1), v + 8);
+      } else {
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+          widen8(e < K ? *reinterpret_cast<const uint4*>(xr + e + 8 * h2) : make_uint4(0, 0, 0, 0),
+                   v + 8 * h2);
+      }
+      stages16<0, (JP < 4 ? JP : 4)>(v);
+      if (JP <= 4) row_max16<RANGE>(v, ma, mb);
+      float* sl = rh + sg * kSegFloats + b1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<float4*>(sl + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    }
+  }
+  if constexpr (JP > 4) {
+    __syncthreads();
+    if (act) {
+      for (int sg = 0; sg < nseg; ++sg) {
+        if (sg * kSeg >= K) continue;
+        float* sl = rh + sg * kSegFloats + b2;
+        float v[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) v[q] = sl[16 * q + 4 * (q >> 2)];
+        stages16<0, (JP < 8 ? JP : 8) - 4>(v);
+        if (JP <= 8) row_max16<RANGE>(v, ma, mb);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) sl[16 * q + 4 * (q >> 2)] = v[q];
+      }
+    }
+  }
+  if constexpr (JP > 8) {
+    __syncthreads();
+    if (act) {
+      for (int sg = 0; sg < nseg; ++sg) {
+        if (sg * kSeg >= K) continue;
+        float* sl = rh + sg * kSegFloats + b3;
+        float v[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) v[q] = sl[272 * q];
+        stages16<0, JP - 8>(v);
+        row_max16<RANGE>(v, ma, mb);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) sl[272 * q] = v[q];
+      }
+    }
+  }
+  if (F28 || (JP == 12 && J > 12)) {
+    // The row maxima are taken in the last pass instead.
+    ma = 0.0f;
+    mb = 0.0f;
+    for (int b = 12; JP == 12 && b < J; ++b) {
+      // Bit b: segments s and s + 2^(b - 12), s with that bit clear.
+      __syncthreads();
+      if (act) {
+        const int S = 1 << (b - 12);
+        const bool last_pass = b == J - 1 && !F28;
+        for (int sg = 0; sg < nseg; ++sg) {
+          if (sg & S) continue;
+          float* lo = rh + sg * kSegFloats + b1;
+          float* hi = lo + S * kSegFloats;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 a = *reinterpret_cast<const float4*>(lo + 4 * q);
+            const float4 c = *reinterpret_cast<const float4*>(hi + 4 * q);
+            const float4 s4 = make_float4(a.x + c.x, a.y + c.y, a.z + c.z, a.w + c.w);
+            const float4 d4 = make_float4(a.x - c.x, a.y - c.y, a.z - c.z, a.w - c.w);
+            *reinterpret_cast<float4*>(lo + 4 * q) = s4;
+            *reinterpret_cast<float4*>(hi + 4 * q) = d4;
+            if (last_pass) {
+              const float o[8] = {s4.x, s4.y, s4.z, s4.w, d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+              for (int u = 0; u < 8; ++u) row_max1<RANGE>(o[u], ma, mb);
+            }
+          }
+        }
+      }
+    }
+    if constexpr (F28) {
+      // y[b p + c] = sum over a = 0..27, in order, of H28[a][b] z[a p + c],
+      // one column (block, c) per thread at a time.
+      __syncthreads();
+      if (act) {
+        const int p = 1 << J;
+        for (int col = r; col < K / 28; col += 256) {
+          const int base = (col >> J) * 28 * p + (col & (p - 1));
+          float z[28];
+#pragma unroll
+          for (int a = 0; a < 28; ++a) z[a] = rh[seg_index(base + a * p)];
+#pragma unroll
+          for (int bb = 0; bb < 28; ++bb) {
+            float acc = kH28.e[0][bb] > 0 ? z[0] : -z[0];
+#pragma unroll
+            for (int a = 1; a < 28; ++a) acc = kH28.e[a][bb] > 0 ? acc + z[a] : acc - z[a];
+            rh[seg_index(base + bb * p)] = acc;
+            row_max1<RANGE>(acc, ma, mb);
+          }
+        }
+      }
+    }
+  }
 }
 
 }  // namespace qd

@@ -279,3 +279,28 @@ def test_fused_decode_validation(L):
     assert call(N=24) == UNSUPPORTED
     assert call(h=3) == INVALID
     assert call(M=0, x=NULL) == OK
+
+
+def test_range_entry_points_validation(L):
+    def rq(M=4, K=4096, h=4096, bits=4, x=FAKE, codes=FAKE, scales=FAKE, zeros=FAKE):
+        return L.dptq_rotate_quant_range(x, M, K, h, bits, codes, scales, zeros, NULL)
+    assert rq(bits=5) == INVALID
+    assert rq(K=4104, h=8) == UNSUPPORTED        # rows must be whole 128-element chunks
+    assert rq(h=3) == INVALID
+    assert rq(zeros=NULL) == INVALID
+    assert rq(codes=MISALIGNED) == INVALID
+    assert rq(M=0, x=NULL) == OK
+    assert L.dptq_weight_sums(FAKE, 4, 48, FAKE, NULL) == UNSUPPORTED
+    assert L.dptq_weight_sums(FAKE, 4, 64, NULL, NULL) == INVALID
+    assert L.dptq_weight_sums(MISALIGNED, 4, 64, FAKE, NULL) == INVALID
+    assert L.dptq_weight_sums(NULL, 0, 64, NULL, NULL) == OK
+
+    def ql(M=4, K=256, bits=4, N=32, acc=FAKE, y=FAKE, sums=FAKE):
+        return L.dptq_qlinear_range(FAKE, FAKE, FAKE, M, K, bits, FAKE, FAKE, sums, N, acc, y, NULL)
+    assert ql(K=200) == UNSUPPORTED
+    assert ql(N=24) == UNSUPPORTED
+    assert ql(bits=6) == INVALID
+    assert ql(acc=NULL) == INVALID
+    assert ql(sums=NULL) == INVALID
+    assert ql(y=MISALIGNED) == INVALID
+    assert ql(M=0, acc=NULL, y=NULL) == OK
