@@ -45,7 +45,8 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=160,
                    help="token rows of the workload the CPU oracle is timed on")
     p.add_argument("--extended", action="store_true",
-                   help="also time the decode shapes and the 28 x 512 rotation")
+                   help="also time the decode shapes, the fused decode, the range quantizer, "
+                        "calibration, KV4 and whole stacks")
     p.add_argument("--only", choices=["rq4", "gemm4", "rq6", "gemm6", "rq8", "gemm8", "copy"],
                    help="run one kernel of the step --steps times (for counter runs) "
                         "or, with copy, a plain device copy of 256 MiB (counter calibration)")
@@ -302,6 +303,81 @@ def time_decode(torch, dptq, args):
     return out
 
 
+def time_decode_fused(torch, dptq):
+    """Decode from fp16 x (rotate + quantize + GEMM) on both paths of the
+    fused entry point and on its automatic choice, at LLaMA decode shapes:
+    graph-replayed launches cycling weight copies beyond the last-level cache.
+    GB/s counts the weights, their scales, x, the codes written and y."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    shapes = [("llama2_7b_qkv", 1, 4096, 12288, 4096), ("llama2_7b_qkv", 2, 4096, 12288, 4096),
+              ("llama2_7b_o", 1, 4096, 4096, 4096), ("llama2_7b_down", 1, 11008, 4096, 256),
+              ("llama3_8b_down", 1, 14336, 4096, 28 * 512), ("llama3_8b_down", 4, 14336, 4096, 28 * 512),
+              ("llama3_8b_down", 16, 14336, 4096, 28 * 512), ("llama2_70b_qkv", 8, 8192, 10240, 8192)]
+    modes = {"auto": dptq.DECODE_AUTO, "one_launch": dptq.DECODE_ONE_LAUNCH,
+             "two_launches": dptq.DECODE_TWO_LAUNCHES}
+    rng = np.random.default_rng(6)
+    out = {}
+    for name, M, K, N, h in shapes:
+        R = max(2, (300 << 20) // (N * K // 2))
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(M + K + N)
+        wps = [torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen)
+               for _ in range(R)]
+        ws = torch.from_numpy(workloads.random_scales(rng, N)).to(dev)
+        x = torch.from_numpy(workloads.student_t(rng, M, K)).to(dev)
+        y = torch.empty((M, N), dtype=torch.float16, device=dev)
+        for bits in (4, 8):
+            codes, scales = dptq.rotate_quant(x, h, bits)
+            nbytes = N * K // 2 + 4 * N + 2 * M * K + M * K * bits // 8 + 4 * M + 2 * M * N
+            rec = {}
+            for mname, mode in modes.items():
+                try:
+                    us = _graph_time(torch, [
+                        (lambda i, mode=mode: (lambda: dptq.qlinear_decode_fused(
+                            x, h, bits, wps[i % R], ws, y, codes, scales, mode=mode)))(i)
+                        for i in range(24)])
+                except dptq.DptqError:
+                    continue          # the rows do not fit on chip for one launch
+                rec[mname] = {"us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
+            out[f"{name}_M{M}_a{bits}"] = rec
+        del wps
+        torch.cuda.empty_cache()
+    return out
+
+
+def time_range(torch, dptq, cfg):
+    """The range quantizer variant (Eq. 1 with a zero point) at the step's
+    shape, next to the symmetric path: rotate + quantize, and the linear
+    (GEMM into the accumulator plus the zero-point epilogue), each timed over
+    24 graph-replayed launches."""
+    import numpy as np
+    import workloads
+    dev = torch.device("cuda:0")
+    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
+    rng = np.random.default_rng(7)
+    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
+    wp = torch.from_numpy(workloads.random_weight_bytes(rng, N, K)).to(dev)
+    ws = torch.from_numpy(workloads.random_scales(rng, N)).to(dev)
+    sums = dptq.weight_sums(wp)
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    acc = torch.empty((M, N), dtype=torch.int32, device=dev)
+    out = {"weight_sums_us": round(_graph_time(torch, [lambda: dptq.weight_sums(wp, sums)] * 24), 2)}
+    for bits in (4, 8):
+        c, s = dptq.rotate_quant(x, h, bits)
+        cr, sr, zr = dptq.rotate_quant_range(x, h, bits)
+        out[f"a{bits}"] = {
+            "rotate_quant_us": round(_graph_time(torch, [lambda: dptq.rotate_quant(x, h, bits, c, s)] * 24), 2),
+            "rotate_quant_range_us": round(_graph_time(
+                torch, [lambda: dptq.rotate_quant_range(x, h, bits, cr, sr, zr)] * 24), 2),
+            "qlinear_us": round(_graph_time(torch, [lambda: dptq.qlinear(c, s, bits, wp, ws, y)] * 24), 2),
+            "qlinear_range_us": round(_graph_time(
+                torch, [lambda: dptq.qlinear_range(cr, sr, zr, bits, wp, ws, sums, y, acc)] * 24), 2),
+        }
+    return out
+
+
 def time_calibration(torch, dptq):
     """Residual-dynamics calibration (Eq. 8-11) of one 4096-wide layer over a
     2048-token batch: per-token JR and SNR plus the layer means, graph-replayed
@@ -505,6 +581,8 @@ def main():
     }
     if args.extended:
         rec["decode"] = time_decode(torch, dptq, args)
+        rec["decode_fused"] = time_decode_fused(torch, dptq)
+        rec["range_quantizer"] = time_range(torch, dptq, cfg)
         rec["calibration"] = time_calibration(torch, dptq)
         rec["kv4"] = time_kv(torch, dptq)
         rec["stacks"] = {"llama2_7b_32_layers": time_stack(torch, dptq, "llama2_7b_stack", (2048, 8)),

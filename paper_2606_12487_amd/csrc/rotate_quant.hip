@@ -442,14 +442,17 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, const uint8_t* signs, ui
   return hipGetLastError();
 }
 
-// Few rows (decode): 1024 threads per row shorten each row's latency; many
-// rows: 256 threads, several rows per compute unit.
+// Few rows (decode), or rows so long that one compute unit's LDS holds only
+// one of them: 1024 threads per row shorten each row's latency and keep 16
+// wavefronts per compute unit.  Many shorter rows: 256 threads, several rows
+// per compute unit.
 constexpr int64_t kFewRows = 64;
+constexpr size_t kOneRowLds = 80 * 1024;
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS, bool FP6>
 hipError_t launch_one(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
                       float* scales, StatsArgs st, hipStream_t stream) {
-  if (M <= kFewRows)
+  if (M <= kFewRows || lds_bytes(K) > kOneRowLds)
     return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, signs, codes, scales, st,
                                                                   stream);
   return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, signs, codes, scales,

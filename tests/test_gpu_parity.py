@@ -76,6 +76,9 @@ ROT_CASES = [
     (2, 11008, 256), (16, 256, 256), (2, 28672, 28 * 512),
     (3, 4096, 512), (2, 16384, 16384), (5, 12288, 4096), (4, 4160, 64),
     (3, 4224, 128), (2, 4104, 8), (3, 4120, 8),
+    # more than 64 rows so long that one compute unit holds one of them
+    # (1024 threads per row, as for decode)
+    (70, 28672, 28 * 1024), (66, 24576, 8192),
 ]
 
 
