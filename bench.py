@@ -579,8 +579,10 @@ def main():
         "rotate_quant_fp6_a4": {"bound": "alu", "GB/s": round(k1_bytes / (rq6_ms * 1e-3) / 1e9, 1),
                                 "frac_of_hbm_peak": round(k1_bytes / (rq6_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
     }
+    # Decode GB/s (the metric's second half): config 3's down projection at
+    # M = 1, 4, 16, a few seconds.
+    rec["decode"] = time_decode(torch, dptq, args)
     if args.extended:
-        rec["decode"] = time_decode(torch, dptq, args)
         rec["decode_fused"] = time_decode_fused(torch, dptq)
         rec["range_quantizer"] = time_range(torch, dptq, cfg)
         rec["calibration"] = time_calibration(torch, dptq)
