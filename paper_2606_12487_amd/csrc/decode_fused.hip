@@ -71,43 +71,48 @@ __device__ __forceinline__ void f_store8(const uint32_t* bt, int e, uint8_t* cl,
   }
 }
 
-// Rotate + quantize rows m0 and, with two rows in flight (rif = 2), m0 + 1:
-// threads 256 * half + r (r < 256) rotate row m0 + half in its own staging
-// (rotate_row_segments), then quantize it into the LDS code rows (and the
-// caller's buffers when given).  p0, p1 with use_pre: this thread's first 16
-// elements of segment 0, loaded by the caller.
-template <int BITS, int JP, bool F28>
+// Rotate + quantize row m0 and, with two rows in flight (!SPLIT), m0 + 1.
+// Two rows: threads 256 * half + r (r < 256) rotate row m0 + half in its own
+// staging.  One row (SPLIT): both groups of 256 work on it, splitting its
+// segments by parity and its 28-point columns.  The row is then quantized
+// into the LDS code rows (and the caller's buffers when given).  pre with
+// use_pre: this thread's first NPRE segments of its work, loaded by the
+// caller.
+template <int BITS, int JP, bool F28, bool SPLIT, int NPRE>
 __device__ __forceinline__ void rows_fast(const __half* __restrict__ x, int M, int K, int J,
-                                          int m0, int rif, bool use_pre, uint4 p0, uint4 p1,
+                                          int m0, bool use_pre, const uint4 (&pre)[2 * NPRE],
                                           float* rot, float* red, uint8_t* cl, int cstride,
                                           float* as_lds, uint8_t* __restrict__ codes_out,
                                           float* __restrict__ scales_out) {
   const int t = threadIdx.x, half = t >> 8, r = t & 255;
-  const int m = m0 + half;
-  const bool act = half < rif && m < M;
+  constexpr bool split = SPLIT;
+  const int m = split ? m0 : m0 + half;
+  const bool act = m < M;
   const int nseg = (K + kSeg - 1) / kSeg;
-  float* rh = rot + half * nseg * kSegFloats;
+  float* rh = split ? rot : rot + half * nseg * kSegFloats;
+  const RowSplit sp = split ? RowSplit{half, 2, t, kFT} : RowSplit{0, 1, r, 256};
   const int b1 = seg_off(16 * r);
   const __half* xr = x + (size_t)m * K;
   float tmax = 0.0f, unused = 0.0f;
-  rotate_row_segments<JP, F28, false>(xr, K, J, act, r, use_pre, p0, p1, rh, tmax, unused);
-  // Row maximum: waves 0-3 hold row m0, waves 4-7 row m0 + 1.
+  rotate_row_segments<JP, F28, false, NPRE>(xr, K, J, act, r, sp, use_pre, pre, rh, tmax, unused);
+  // Row maximum: waves 0-3 hold row m0, waves 4-7 row m0 + 1 (or row m0 too).
   tmax = wave_max_nonneg(tmax);
   if ((t & 63) == 0) red[t >> 6] = tmax;
   __syncthreads();
-  const float* rr = red + 4 * half;
-  const float amax = fmaxf(fmaxf(rr[0], rr[1]), fmaxf(rr[2], rr[3]));
+  const float* rr = red + (split ? 0 : 4 * half);
+  float amax = fmaxf(fmaxf(rr[0], rr[1]), fmaxf(rr[2], rr[3]));
+  if (split) amax = fmaxf(amax, fmaxf(fmaxf(red[4], red[5]), fmaxf(red[6], red[7])));
   constexpr float qmax = (float)((1 << (BITS - 1)) - 1);
   const float sc = amax / qmax;                 // IEEE division
   const float rc = sc != 0.0f ? 1.0f / sc : 0.0f;
   if (act) {
-    if (r == 0) {
+    if (t == 0 || (!split && r == 0)) {
       as_lds[m] = sc;
       if (scales_out) scales_out[m] = sc;
     }
     uint8_t* crow = cl + (size_t)m * cstride;
     uint8_t* grow = codes_out ? codes_out + (size_t)m * (BITS == 4 ? K / 2 : K) : nullptr;
-    for (int sg = 0; sg < nseg; ++sg) {
+    for (int sg = sp.sg0; sg < nseg; sg += sp.sgstep) {
       const int e = sg * kSeg + 16 * r;
       if (e >= K) continue;
       const float* sl = rh + sg * kSegFloats + b1;
@@ -127,18 +132,21 @@ __device__ __forceinline__ void rows_fast(const __half* __restrict__ x, int M, i
   __syncthreads();   // the staging and red[] are reused by the next rows
 }
 
-// h = F * 2^J with JP = min(J, 12), F28 = (F == 28).  Dynamic LDS: the M code rows (row
-// stride cstride = K * BITS / 8 + 16 bytes), then the fp32 staging of rif rows.
-template <int BITS, int JP, bool F28>
-__global__ void __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(F28 ? 4 : 6)))
-qdecode_fused(const __half* __restrict__ x, int M, int K, int J, int rif,
+// h = F * 2^J with JP = min(J, 12), F28 = (F == 28); SPLIT: one row at a time
+// on all 512 threads, else two rows in flight.  Dynamic LDS: the M code rows
+// (row stride cstride = K * BITS / 8 + 16 bytes), then the fp32 staging of one
+// row (SPLIT) or two.
+template <int BITS, int JP, bool F28, bool SPLIT>
+__global__ void __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(F28 ? 2 : 6)))
+qdecode_fused(const __half* __restrict__ x, int M, int K, int J,
               const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales, int N,
               __half* __restrict__ y, uint8_t* __restrict__ codes_out, float* __restrict__ scales_out) {
   extern __shared__ __align__(16) uint8_t dyn[];
   __shared__ float red[kFWaves];
   __shared__ float as_lds[16];
   __shared__ v4i_t part[kFWaves][64];
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // uniform: scalar chunk bounds
   __builtin_assume(M >= 1 && M <= 16);   // the launcher's range
   const int cstride = K * BITS / 8 + 16;
   uint8_t* cl = dyn;
@@ -161,63 +169,77 @@ qdecode_fused(const __half* __restrict__ x, int M, int K, int J, int rif,
   // Loads are unconditional (addresses clamped into the buffers, values past
   // the range replaced by zero afterwards): no branch around a load, so the
   // waits before the rotation cover only the activation loads.
-  const uint4 z4 = make_uint4(0, 0, 0, 0);
-  uint4 pre[2] = {z4, z4};
+  // This thread's activation segments (the first kPreSeg of its first row),
+  // then the weights: the rotation then waits for the activations alone.
+  // The 28-point instances, whose rows are long, preload four segments.
+  constexpr int kPreSeg = F28 ? 4 : 1;
+  uint4 pre[2 * kPreSeg];
   {
-    const int half = t >> 8, e = 16 * (t & 255);
-    const bool ok = half < rif && half < M && e < K;
-    const __half* xp = ok ? x + (size_t)half * K + e : x;
+    // The segments rows_fast gives this thread in its first call: row half
+    // from segment 0 (two rows in flight), or row 0 from segment half in
+    // steps of two (one row, both groups on it).
+    const int half = t >> 8, r = t & 255;
+    const int row = SPLIT ? 0 : half, sg0 = SPLIT ? half : 0, sgstep = SPLIT ? 2 : 1;
+    const bool ok = row < M;
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      pre[h2] = *reinterpret_cast<const uint4*>(xp + 8 * h2);
+    for (int i = 0; i < kPreSeg; ++i) {
+      const int e = (sg0 + i * sgstep) * kSeg + 16 * r;
+      const __half* xp = ok && e < K ? x + (size_t)row * K + e : x;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) pre[2 * i + h2] = *reinterpret_cast<const uint4*>(xp + 8 * h2);
     }
     __builtin_amdgcn_sched_barrier(0);   // the activation loads go out first
   }
   const int last = nck - 1;
-  uint4 wv[kFBatch];
+  // Weights prefetched before the rotation: one batch, or for the 28-point
+  // stage (whose rotation takes longest) up to 16 chunks, the whole slice of
+  // a wavefront at K <= 16384.  Raw loads; values past the wavefront's
+  // chunks are zeroed at use.
+  constexpr int kPF = F28 ? 16 : kFBatch;
+  uint4 wpre[kPF];
 #pragma unroll
-  for (int k = 0; k < kFBatch; ++k) {
-    const int ck = c_begin + k;
-    const uint4 u = *reinterpret_cast<const uint4*>(wp + (size_t)min(ck, last) * 64);
-    wv[k] = keep_or_zero(ck < c_end, u);
-  }
+  for (int k = 0; k < kPF; ++k)
+    wpre[k] = *reinterpret_cast<const uint4*>(wp + (size_t)min(c_begin + k, last) * 64);
   __builtin_amdgcn_sched_barrier(0);     // ... then the weights, then the rotation
 
-  for (int m0 = 0; m0 < M; m0 += rif)
-    rows_fast<BITS, JP, F28>(x, M, K, J, m0, rif, m0 == 0, pre[0], pre[1], rot, red, cl, cstride, as_lds,
-                        cg, sgl);
+  for (int m0 = 0; m0 < M; m0 += SPLIT ? 1 : 2)
+    rows_fast<BITS, JP, F28, SPLIT, kPreSeg>(x, M, K, J, m0, m0 == 0, pre, rot, red, cl, cstride,
+                                             as_lds, cg, sgl);
 
   const uint8_t* ap = cl + (size_t)(mvalid ? fr : 0) * cstride + (BITS == 4 ? fg * 16 : fg * 32);
   v4i_t acc = v4i_t{0, 0, 0, 0};
-  for (int c = c_begin; c < c_end; c += kFBatch) {
-    if (c != c_begin) {
-#pragma unroll
-      for (int k = 0; k < kFBatch; ++k) {
-        const int ck = c + k;
-        const uint4 u = *reinterpret_cast<const uint4*>(wp + (size_t)min(ck, last) * 64);
-        wv[k] = keep_or_zero(ck < c_end, u);
-      }
+  // Chunk ck (c_begin <= ck, and some chunk of this wavefront exists) with
+  // its weights w; the codes come from LDS chunk by chunk.
+  auto consume = [&](int ck, uint4 w) __attribute__((always_inline)) {
+    const bool in = ck < c_end;
+    const bool ok = in && mvalid;
+    const int cc = min(ck, c_end - 1);
+    w = keep_or_zero(in, w);
+    v4i_t b0, b1;
+    if (BITS == 4) {
+      const uint4 u = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 64));
+      b0 = f_op_nibbles(u.x, u.y);
+      b1 = f_op_nibbles(u.z, u.w);
+    } else {
+      const uint4 u = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128));
+      const uint4 u2 = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128 + 16));
+      b0 = f_op_bytes(u.x, u.y, u.z, u.w);
+      b1 = f_op_bytes(u2.x, u2.y, u2.z, u2.w);
     }
-    // The codes come from LDS chunk by chunk (short latency, few registers).
+    acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(f_op_nibbles(w.x, w.y), b0, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(f_op_nibbles(w.z, w.w), b1, acc, 0, 0, 0);
+  };
+  if (c_begin < c_end) {
 #pragma unroll
-    for (int k = 0; k < kFBatch; ++k) {
-      const int ck = c + k;
-      const bool ok = ck < c_end && mvalid;
-      const int cc = min(ck, c_end - 1);   // c < c_end: a chunk of this wavefront
-      v4i_t b0, b1;
-      if (BITS == 4) {
-        const uint4 u = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 64));
-        b0 = f_op_nibbles(u.x, u.y);
-        b1 = f_op_nibbles(u.z, u.w);
-      } else {
-        const uint4 u = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128));
-        const uint4 u2 = keep_or_zero(ok, *reinterpret_cast<const uint4*>(ap + (size_t)cc * 128 + 16));
-        b0 = f_op_bytes(u.x, u.y, u.z, u.w);
-        b1 = f_op_bytes(u2.x, u2.y, u2.z, u2.w);
-      }
-      acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(f_op_nibbles(wv[k].x, wv[k].y), b0, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(f_op_nibbles(wv[k].z, wv[k].w), b1, acc, 0, 0, 0);
-    }
+    for (int k = 0; k < kPF; ++k) consume(c_begin + k, wpre[k]);
+  }
+  for (int c = c_begin + kPF; c < c_end; c += kFBatch) {
+    uint4 wv[kFBatch];
+#pragma unroll
+    for (int k = 0; k < kFBatch; ++k)
+      wv[k] = *reinterpret_cast<const uint4*>(wp + (size_t)min(c + k, last) * 64);
+#pragma unroll
+    for (int k = 0; k < kFBatch; ++k) consume(c + k, wv[k]);
   }
   part[wave][lane] = acc;
   __syncthreads();
@@ -247,13 +269,11 @@ int64_t staging_bytes(int K) { return (int64_t)((K + kSeg - 1) / kSeg) * kSegFlo
 
 int64_t code_rows_bytes(int64_t M, int K, int bits) { return M * ((int64_t)K * bits / 8 + 16); }
 
-template <int BITS, int JP, bool F28>
-hipError_t launch_fused_t(const void* x, int64_t M, int K, HadSplit hs, const uint8_t* w,
-                          const float* ws, int64_t N, void* y, void* codes, float* as,
-                          hipStream_t stream) {
-  auto kern = qdecode_fused<BITS, JP, F28>;
-  const int64_t rows = code_rows_bytes(M, K, BITS), stage = staging_bytes(K);
-  const int rif = M >= 2 && rows + 2 * stage <= kFusedLdsMax ? 2 : 1;
+template <int BITS, int JP, bool F28, bool SPLIT>
+hipError_t launch_fused_split(const void* x, int64_t M, int K, HadSplit hs, const uint8_t* w,
+                              const float* ws, int64_t N, void* y, void* codes, float* as,
+                              size_t lds, hipStream_t stream) {
+  auto kern = qdecode_fused<BITS, JP, F28, SPLIT>;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -261,10 +281,24 @@ hipError_t launch_fused_t(const void* x, int64_t M, int K, HadSplit hs, const ui
     (void)hipGetLastError();
     attr_set = true;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)(N / 16)), dim3(kFT), (size_t)(rows + rif * stage), stream,
-                     static_cast<const __half*>(x), (int)M, K, hs.j, rif, w, ws, (int)N,
+  hipLaunchKernelGGL(kern, dim3((unsigned)(N / 16)), dim3(kFT), lds, stream,
+                     static_cast<const __half*>(x), (int)M, K, hs.j, w, ws, (int)N,
                      static_cast<__half*>(y), static_cast<uint8_t*>(codes), as);
   return hipGetLastError();
+}
+
+// Two rows in flight when M >= 2 and both stagings fit; else one row at a
+// time on all threads.
+template <int BITS, int JP, bool F28>
+hipError_t launch_fused_t(const void* x, int64_t M, int K, HadSplit hs, const uint8_t* w,
+                          const float* ws, int64_t N, void* y, void* codes, float* as,
+                          hipStream_t stream) {
+  const int64_t rows = code_rows_bytes(M, K, BITS), stage = staging_bytes(K);
+  if (M >= 2 && rows + 2 * stage <= kFusedLdsMax)
+    return launch_fused_split<BITS, JP, F28, false>(x, M, K, hs, w, ws, N, y, codes, as,
+                                                    (size_t)(rows + 2 * stage), stream);
+  return launch_fused_split<BITS, JP, F28, true>(x, M, K, hs, w, ws, N, y, codes, as,
+                                                 (size_t)(rows + stage), stream);
 }
 
 // h = 28 * 2^j has j <= 10 (h <= the longest row); h = 2^j goes to JP = min(j, 12).
@@ -293,14 +327,15 @@ int64_t decode_fused_lds(int64_t M, int K, HadSplit hs, int bits) {
 }
 
 // Measured on decode shapes: the repeated rotation costs less than the
-// second launch for one or two rows of power-of-two blocks of at most 4096
-// (one row at h = 8192), K <= 12288, and at most 1024 workgroups (about
-// three per compute unit, so each rotates once); more rows, longer rows, the
-// 28-point stage or more workgroups make it the slower path.
+// second launch for one row of K <= 16384 with h = 2^j <= 8192, or of
+// K <= 14336 with h = 28 * 2^j, and for two rows of K <= 12288 with
+// h = 2^j <= 4096; in every case for at most 1024 workgroups (about three
+// per compute unit, so each rotates once).  More rows, longer rows or more
+// workgroups make it the slower path.
 bool decode_one_launch_wins(int64_t M, int K, HadSplit hs, int bits, int64_t N) {
-  if (hs.f != 1 || K > 12288 || N > 16384 || M > 2) return false;
-  if (hs.j > 12 && (M > 1 || hs.j > 13)) return false;
-  return decode_fused_lds(M, K, hs, bits) <= kFusedLdsMax;
+  if (N > 16384 || decode_fused_lds(M, K, hs, bits) > kFusedLdsMax) return false;
+  if (M == 1) return hs.f == 28 ? K <= 14336 : (hs.j <= 13 && K <= 16384);
+  return M == 2 && hs.f == 1 && hs.j <= 12 && K <= 12288;
 }
 
 hipError_t launch_decode_fused(const void* x, int64_t M, int K, HadSplit hs, int bits,

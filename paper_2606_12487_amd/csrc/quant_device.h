@@ -121,9 +121,11 @@ __device__ __forceinline__ float wave_max_nonneg(float m) {
 // slow index.  K is a multiple of 128, so a thread's 16 elements are all in
 // the row or all past it; past the row end the segment is zero (whole
 // Hadamard blocks of zeros).  The rotated row is left in rh (element i at
-// seg_index(i)).  Every thread of the workgroup calls this (it holds
-// barriers); act = false threads only join them.  With use_pre, p0 and p1 are
-// this thread's first 16 elements of segment 0, loaded by the caller.
+// seg_index(i)).  r is the thread's place in its group of 256 (its part of a
+// segment), sp how the row's work is shared.  Every thread of the workgroup
+// calls this (it holds barriers); act = false threads only join them.  With use_pre, pre[2 sg] and
+// pre[2 sg + 1] are this thread's 16 elements of segment sg < NPRE, loaded by
+// the caller (any values where they lie past the row end).
 //
 // Row maxima, each starting at 0: RANGE = false keeps the absolute maximum
 // in ma; RANGE = true keeps max(0, max v) in ma and max(0, max -v) in mb.
@@ -165,39 +167,65 @@ __device__ __forceinline__ void row_max16(const float* v, float& ma, float& mb) 
   }
 }
 
-template <int JP, bool F28, bool RANGE>
+// How the threads of a row share its work: segments sg0, sg0 + sgstep, ... in
+// the register phases and the passes across segments, and columns tid,
+// tid + nthr, ... in the 28-point pass.  One group of 256 threads per row is
+// {0, 1, r, 256}; two groups on one row split the segments by parity.
+struct RowSplit {
+  int sg0, sgstep, tid, nthr;
+};
+
+template <int JP, bool F28, bool RANGE, int NPRE>
 __device__ __forceinline__ void rotate_row_segments(const __half* __restrict__ xr, int K, int J,
-                                                    bool act, int r, bool use_pre, uint4 p0,
-                                                    uint4 p1, float* rh, float& ma, float& mb) {
+                                                    bool act, int r, RowSplit sp, bool use_pre,
+                                                    const uint4 (&pre)[2 * NPRE], float* rh,
+                                                    float& ma, float& mb) {
   const int nseg = (K + kSeg - 1) / kSeg;
   const int b1 = seg_off(16 * r);
   const int b2 = seg_off(256 * (r >> 4) + (r & 15));
   const int b3 = seg_off(r);
+  // Phase 1 of segment sg from its 16 fp16 values (zero past the row end).
+  auto phase1 = [&](int sg, uint4 u0, uint4 u1) __attribute__((always_inline)) {
+    const bool in = sg * kSeg + 16 * r < K;
+    float v[16];
+    widen8(keep_or_zero(in, u0), v);
+    widen8(keep_or_zero(in, u1), v + 8);
+    stages16<0, (JP < 4 ? JP : 4)>(v);
+    if (JP <= 4) row_max16<RANGE>(v, ma, mb);
+    float* sl = rh + sg * kSegFloats + b1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<float4*>(sl + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  };
+  auto load16 = [&](int sg, int h2) __attribute__((always_inline)) {
+    const int e = sg * kSeg + 16 * r;
+    return e < K ? *reinterpret_cast<const uint4*>(xr + e + 8 * h2) : make_uint4(0, 0, 0, 0);
+  };
   if (act) {
-    for (int sg = 0; sg < nseg; ++sg) {
-      const int e = sg * kSeg + 16 * r;
-      float v[16];
-      if (use_pre && sg == 0) {
-        widen8(keep_or_zero(e < K, p0), v);
-        widen8(keep_or_zero(e < K, p1), v + 8);
-      } else {
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2)
-          widen8(e < K ? *reinterpret_cast<const uint4*>(xr + e + 8 * h2) : make_uint4(0, 0, 0, 0),
-                   v + 8 * h2);
+    // The first NPRE segments may come preloaded (the caller issued those
+    // loads before others it wants to stay in flight).
+    if constexpr (NPRE == 1) {
+      for (int sg = sp.sg0; sg < nseg; sg += sp.sgstep) {
+        if (use_pre && sg == sp.sg0) phase1(sg, pre[0], pre[1]);
+        else phase1(sg, load16(sg, 0), load16(sg, 1));
       }
-      stages16<0, (JP < 4 ? JP : 4)>(v);
-      if (JP <= 4) row_max16<RANGE>(v, ma, mb);
-      float* sl = rh + sg * kSegFloats + b1;
+    } else {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<float4*>(sl + 4 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+      for (int i = 0; i < NPRE; ++i) {
+        const int sg = sp.sg0 + i * sp.sgstep;
+        if (sg < nseg) {
+          if (use_pre) phase1(sg, pre[2 * i], pre[2 * i + 1]);
+          else phase1(sg, load16(sg, 0), load16(sg, 1));
+        }
+      }
+      for (int sg = sp.sg0 + NPRE * sp.sgstep; sg < nseg; sg += sp.sgstep)
+        phase1(sg, load16(sg, 0), load16(sg, 1));
     }
   }
   if constexpr (JP > 4) {
     __syncthreads();
     if (act) {
-      for (int sg = 0; sg < nseg; ++sg) {
+      for (int sg = sp.sg0; sg < nseg; sg += sp.sgstep) {
         if (sg * kSeg >= K) continue;
         float* sl = rh + sg * kSegFloats + b2;
         float v[16];
@@ -213,7 +241,7 @@ __device__ __forceinline__ void rotate_row_segments(const __half* __restrict__ x
   if constexpr (JP > 8) {
     __syncthreads();
     if (act) {
-      for (int sg = 0; sg < nseg; ++sg) {
+      for (int sg = sp.sg0; sg < nseg; sg += sp.sgstep) {
         if (sg * kSeg >= K) continue;
         float* sl = rh + sg * kSegFloats + b3;
         float v[16];
@@ -236,8 +264,9 @@ __device__ __forceinline__ void rotate_row_segments(const __half* __restrict__ x
       if (act) {
         const int S = 1 << (b - 12);
         const bool last_pass = b == J - 1 && !F28;
-        for (int sg = 0; sg < nseg; ++sg) {
-          if (sg & S) continue;
+        // Pair p: the segment with bit b - 12 inserted as 0, and its partner.
+        for (int p = sp.sg0; p < nseg / 2; p += sp.sgstep) {
+          const int sg = ((p >> (b - 12)) << (b - 11)) | (p & (S - 1));
           float* lo = rh + sg * kSegFloats + b1;
           float* hi = lo + S * kSegFloats;
 #pragma unroll
@@ -263,7 +292,7 @@ __device__ __forceinline__ void rotate_row_segments(const __half* __restrict__ x
       __syncthreads();
       if (act) {
         const int p = 1 << J;
-        for (int col = r; col < K / 28; col += 256) {
+        for (int col = sp.tid; col < K / 28; col += sp.nthr) {
           const int base = (col >> J) * 28 * p + (col & (p - 1));
           float z[28];
 #pragma unroll

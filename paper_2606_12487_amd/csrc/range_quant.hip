@@ -34,9 +34,10 @@ rq_range_kernel(const __half* __restrict__ x, int K, int J, uint8_t* __restrict_
   extern __shared__ float lds[];
   __shared__ float red[2][kRT / 64];
   const int row = blockIdx.x, r = threadIdx.x;
-  const uint4 z4 = make_uint4(0, 0, 0, 0);
+  const uint4 none[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
   float hi = 0.0f, neg = 0.0f;
-  rotate_row_segments<JP, F28, true>(x + (size_t)row * K, K, J, true, r, false, z4, z4, lds, hi, neg);
+  rotate_row_segments<JP, F28, true, 1>(x + (size_t)row * K, K, J, true, r, RowSplit{0, 1, r, kRT},
+                                        false, none, lds, hi, neg);
   hi = wave_max_nonneg(hi);
   neg = wave_max_nonneg(neg);
   if ((r & 63) == 0) {
