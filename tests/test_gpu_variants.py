@@ -116,6 +116,9 @@ FUSED_CASES = [
     (16, 1024, 16, 1024, 8), (16, 4096, 12288, 4096, 8), (16, 11008, 4096, 256, 4),
     (5, 6144, 256, 2048, 8), (2, 7168, 512, 28 * 256, 8), (1, 28672, 64, 28 * 1024, 4),
     (3, 896, 32, 28, 8), (2, 16384, 64, 16384, 8), (1, 14336, 4096, 28 * 512, 8),
+    # one row on both thread groups: segments split by parity (2 and 3 of
+    # them), and three rows that do not fit two at a time
+    (1, 8192, 256, 8192, 4), (1, 11008, 256, 256, 8), (3, 14336, 128, 28 * 512, 4),
 ]
 # Shapes whose rows do not fit on chip: the two-launch path only.
 TWO_LAUNCH_ONLY = [(16, 14336, 4096, 28 * 512, 8), (8, 28672, 256, 28 * 1024, 4),
@@ -150,7 +153,7 @@ def test_fused_decode_two_launches_matches_oracle(dev, M, K, N, h, bits):
 
 
 @pytest.mark.parametrize("M,K,N,h,bits", [(1, 4096, 4096, 4096, 4), (2, 8192, 512, 8192, 8),
-                                          (16, 14336, 512, 28 * 512, 8)])
+                                          (16, 14336, 512, 28 * 512, 8), (1, 14336, 512, 28 * 512, 4)])
 def test_fused_decode_auto_matches_oracle(dev, M, K, N, h, bits):
     _fused_case(dev, M, K, N, h, bits, dptq.DECODE_AUTO)
 
