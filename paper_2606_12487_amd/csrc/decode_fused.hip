@@ -164,14 +164,12 @@ qdecode_fused(const __half* __restrict__ x, int M, int K, int J,
   const bool mvalid = fr < M;
   const uint8_t* wp = w_packed + (size_t)(n0 + fr) * (K / 2) + fg * 16;
 
-  // This thread's first activation elements, then the first weight batch:
-  // both are in flight while the rotation starts.
-  // Loads are unconditional (addresses clamped into the buffers, values past
-  // the range replaced by zero afterwards): no branch around a load, so the
-  // waits before the rotation cover only the activation loads.
   // This thread's activation segments (the first kPreSeg of its first row),
-  // then the weights: the rotation then waits for the activations alone.
-  // The 28-point instances, whose rows are long, preload four segments.
+  // then its first weights: the rotation waits for the activations alone while
+  // the weights stay in flight.  Loads are unconditional (addresses clamped
+  // into the buffers, values past the range zeroed at use), so no branch
+  // around a load forces an early wait.  The 28-point instances, whose rows
+  // are long, preload four segments.
   constexpr int kPreSeg = F28 ? 4 : 1;
   uint4 pre[2 * kPreSeg];
   {
