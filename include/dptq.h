@@ -12,6 +12,13 @@
  *      (Y = X W^T, Section 2; weights pre-rotated offline, Eq. 5), followed by
  *      a per-token x per-channel dequant epilogue.
  *
+ * Around it: the residual-dynamics calibration statistics and the layer rule
+ * of Section 3 (Eq. 8-11, 20), the group-wise 4-bit KV-cache codec
+ * (Section 4.2), the same 4-bit x 4-bit product on the FP6 matrix cores,
+ * and variants of the path: randomized-sign (QuaRot-style) rotation, decode
+ * from fp16 activations in one launch, and the range quantizer of Eq. 1 with
+ * a zero point.
+ *
  * Conventions shared by every entry point
  *   - Every pointer named "device" is GPU memory owned by the caller; the
  *     library never allocates, frees or retains memory and keeps no state
