@@ -439,7 +439,11 @@ def time_stack(torch, dptq, name, Ms, reps=3):
     code bytes drawn on the device: the time does not depend on their values);
     each linear's input is the seeded stack input of a mid-stack layer.
     Returns ms per stack for all-4-bit, the paper's default set, a seeded
-    4-layer mask and all-8-bit activations, and the mixed/all-4-bit ratios."""
+    4-layer mask and all-8-bit activations, and the mixed/all-4-bit ratios.
+    At prefill sizes the same policies run again with the 4-bit layers on the
+    FP6 path (rotate+quantize into the FP6 layout, FP6 GEMM against weights
+    packed once into it) and the 8-bit layers on the int8 path: the "_fp6"
+    entries."""
     import workloads
     dev = torch.device("cuda:0")
     cfg = workloads.CONFIGS[name]
@@ -454,6 +458,9 @@ def time_stack(torch, dptq, name, Ms, reps=3):
                 "seeded_mask": dptq.layer_policy(L, workloads.layer_mask(L, 4, cfg["mask_seed"])),
                 "all_a8": [8] * L}
     out = {"weights_GB": round(wbytes / 1e9, 2)}
+    W6 = None
+    if any(M > 16 for M in Ms):
+        W6 = [[dptq.pack_fp6(W[l][i][0]) for i in range(len(lins))] for l in range(L)]
     for M in Ms:
         X = [torch.from_numpy(workloads.stack_layer_input(name, L // 2, n, M=M)).to(dev)
              for n, *_ in lins]
@@ -474,15 +481,40 @@ def time_stack(torch, dptq, name, Ms, reps=3):
                         dptq.qlinear(codes, sbuf, b, W[l][i][0], W[l][i][1],
                                      ybuf[: M * N].view(M, N))
             res[pname] = _graph_time(torch, [run], reps=reps) / 1e3
+        if M > 16:
+            a6buf = torch.empty(max(dptq.fp6_bytes(M, K) for _, K, _, _ in lins), dtype=torch.uint8,
+                                device=dev)
+            for pname in ("all_a4", "default", "seeded_mask"):
+                bits = policies[pname]
+
+                def run6(bits=bits):
+                    for l in range(L):
+                        b = bits[l]
+                        for i, (_, K, N, h) in enumerate(lins):
+                            y = ybuf[: M * N].view(M, N)
+                            if b == 4:
+                                a6 = a6buf[: dptq.fp6_bytes(M, K)]
+                                dptq.rotate_quant_fp6(X[i], h, a6, sbuf)
+                                dptq.qlinear_fp6(a6, sbuf, W6[l][i], W[l][i][1], M, K, N, y)
+                            else:
+                                codes = cbuf[: M * K].view(torch.int8).view(M, K)
+                                dptq.rotate_quant(X[i], h, 8, codes, sbuf)
+                                dptq.qlinear(codes, sbuf, 8, W[l][i][0], W[l][i][1], y)
+                res[pname + "_fp6"] = _graph_time(torch, [run6], reps=reps) / 1e3
+            del a6buf
         ops = 2.0 * M * sum(K * N for _, K, N, _ in lins) * L
         ent = {f"{p}_ms": round(v, 3) for p, v in res.items()}
         ent["default_over_all_a4"] = round(res["default"] / res["all_a4"], 4)
         ent["seeded_mask_over_all_a4"] = round(res["seeded_mask"] / res["all_a4"], 4)
         ent["all_a4_TOPS"] = round(ops / (res["all_a4"] * 1e-3) / 1e12, 1)
         ent["all_a4_weight_GB/s"] = round(wbytes / (res["all_a4"] * 1e-3) / 1e9, 1)
+        if "all_a4_fp6" in res:
+            ent["default_fp6_over_all_a4_fp6"] = round(res["default_fp6"] / res["all_a4_fp6"], 4)
+            ent["seeded_mask_fp6_over_all_a4_fp6"] = round(res["seeded_mask_fp6"] / res["all_a4_fp6"], 4)
+            ent["all_a4_fp6_TOPS"] = round(ops / (res["all_a4_fp6"] * 1e-3) / 1e12, 1)
         out[f"M{M}"] = ent
         del X, cbuf, ybuf
-    del W
+    del W, W6
     torch.cuda.empty_cache()
     return out
 
