@@ -437,7 +437,9 @@ def time_stack(torch, dptq, name, Ms, reps=3):
     and GEMM per linear, layer bits from the policy), captured as one HIP graph
     per policy and replayed.  Each layer has its own weights (random packed
     code bytes drawn on the device: the time does not depend on their values);
-    each linear's input is the seeded stack input of a mid-stack layer.
+    each linear's input is the seeded stack input of a mid-stack layer.  At
+    decode sizes (M <= 16) each linear is one call of the decode entry point,
+    which picks one launch or two.
     Returns ms per stack for all-4-bit, the paper's default set, a seeded
     4-layer mask and all-8-bit activations, and the mixed/all-4-bit ratios.
     At prefill sizes the same policies run again with the 4-bit layers on the
@@ -477,9 +479,13 @@ def time_stack(torch, dptq, name, Ms, reps=3):
                     for i, (_, K, N, h) in enumerate(lins):
                         dt = torch.uint8 if b == 4 else torch.int8
                         codes = cbuf[: M * K * b // 8].view(dt).view(M, K * b // 8)
-                        dptq.rotate_quant(X[i], h, b, codes, sbuf)
-                        dptq.qlinear(codes, sbuf, b, W[l][i][0], W[l][i][1],
-                                     ybuf[: M * N].view(M, N))
+                        y = ybuf[: M * N].view(M, N)
+                        if M <= 16:   # the decode entry point's own choice of path
+                            dptq.qlinear_decode_fused(X[i], h, b, W[l][i][0], W[l][i][1], y, codes,
+                                                      sbuf, mode=dptq.DECODE_AUTO)
+                        else:
+                            dptq.rotate_quant(X[i], h, b, codes, sbuf)
+                            dptq.qlinear(codes, sbuf, b, W[l][i][0], W[l][i][1], y)
             res[pname] = _graph_time(torch, [run], reps=reps) / 1e3
         if M > 16:
             a6buf = torch.empty(max(dptq.fp6_bytes(M, K) for _, K, _, _ in lins), dtype=torch.uint8,
@@ -619,8 +625,8 @@ def main():
         rec["range_quantizer"] = time_range(torch, dptq, cfg)
         rec["calibration"] = time_calibration(torch, dptq)
         rec["kv4"] = time_kv(torch, dptq)
-        rec["stacks"] = {"llama2_7b_32_layers": time_stack(torch, dptq, "llama2_7b_stack", (2048, 8)),
-                         "llama2_70b_80_layers": time_stack(torch, dptq, "llama2_70b_layer", (4096, 8))}
+        rec["stacks"] = {"llama2_7b_32_layers": time_stack(torch, dptq, "llama2_7b_stack", (2048, 8, 1)),
+                         "llama2_70b_80_layers": time_stack(torch, dptq, "llama2_70b_layer", (4096, 8, 1))}
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(cfg, args.cpu_rows)
     print(json.dumps(rec), flush=True)
