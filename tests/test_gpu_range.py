@@ -42,6 +42,9 @@ RQ_CASES = [
     # blocks of 256
     (5, 128, 8), (16, 256, 256), (33, 4096, 4096), (9, 6144, 2048), (3, 16384, 16384),
     (7, 896, 28), (4, 14336, 28 * 512), (2, 28672, 28 * 1024), (6, 11008, 256),
+    # the longest row (nine segments, the largest staging) and a batch of
+    # more rows than compute units
+    (2, 36864, 4096), (300, 1024, 1024),
 ]
 
 
