@@ -64,7 +64,7 @@ def source_digest(path):
 
 
 def measured_traffic():
-    """HBM bytes per launch of the A4 GEMM from the committed counter summary,
+    """HBM bytes per launch of the A8 int8 GEMM from the committed counter summary,
     or None when it is missing or was taken on a different kernel source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None

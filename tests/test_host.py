@@ -1,0 +1,43 @@
+"""Host-side logic around the library (CPU only): the benchmark's contract
+checks, its counter-summary guard, and the build/smoke entry module."""
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    # One GPU only: the request for more exits with status 2 and says why,
+    # before anything touches a device.
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_bench_traffic_is_tied_to_the_kernel_source(tmp_path, monkeypatch):
+    import bench
+    # The committed summary names the digest of the kernel source it was
+    # measured on; a summary for any other source is not used.
+    got = bench.measured_traffic()
+    assert got is None or got > 0
+    fake = tmp_path / "traffic.txt"
+    fake.write_text("source_sha256_16: 0000000000000000\nhbm_bytes_per_launch: 123\n")
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(fake))
+    assert bench.measured_traffic() is None
+    fake.write_text(f"source_sha256_16: {bench.source_digest(bench.KERNEL_SOURCE)}\n"
+                    "hbm_bytes_per_launch: 123\n")
+    assert bench.measured_traffic() == 123
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.txt"))
+    assert bench.measured_traffic() is None
+
+
+def test_entry_module_has_build_and_smoke():
+    import __graft_entry__ as g
+    assert callable(g.build) and callable(g.smoke)
