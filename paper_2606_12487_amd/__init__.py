@@ -532,7 +532,8 @@ def weight_sums(w_packed, out=None):
 
 def qlinear_range(codes, scales, zeros, bits, w_packed, w_scales, w_sums, y=None, acc=None):
     """Quantized linear on range-quantized activations (zero-point corrected).
-    Returns y [M, N] fp16; acc (int32 [M, N] workspace) holds the raw accumulator."""
+    Returns y [M, N] fp16; for M > 16, acc (int32 [M, N] workspace) holds the
+    raw accumulator afterwards."""
     torch = _torch()
     M = scales.shape[0]
     N, K2 = w_packed.shape
@@ -545,10 +546,11 @@ def qlinear_range(codes, scales, zeros, bits, w_packed, w_scales, w_sums, y=None
     _require(w_sums, "w_sums", torch.int32, (N,))
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
-    if acc is None:
+    if acc is None and M > 16:   # decode shapes need no workspace
         acc = torch.empty((M, N), dtype=torch.int32, device=codes.device)
     _require(y, "y", torch.float16, (M, N))
-    _require(acc, "acc", torch.int32, (M, N))
+    if acc is not None:
+        _require(acc, "acc", torch.int32, (M, N))
     _check(lib().dptq_qlinear_range(_ptr(codes), _ptr(scales), _ptr(zeros), M, K, int(bits),
                                     _ptr(w_packed), _ptr(w_scales), _ptr(w_sums), N, _ptr(acc),
                                     _ptr(y), _stream(codes)), "dptq_qlinear_range")

@@ -322,12 +322,17 @@ int dptq_qlinear_range(const void* codes, const float* a_scales, const int32_t* 
   int st = check_gemm_shape(M, K, bits, N);
   if (st != DPTQ_OK) return st;
   if (M == 0) return DPTQ_OK;
-  if (!codes || !a_scales || !a_zeros || !w_packed || !w_scales || !w_sums || !acc || !y)
+  const bool decode = M <= 16;   // one launch, the correction in the decode GEMM's epilogue
+  if (!codes || !a_scales || !a_zeros || !w_packed || !w_scales || !w_sums || !y ||
+      (!decode && !acc))
     return DPTQ_ERR_INVALID_ARG;
   if (!aligned16(codes) || !aligned4(a_scales) || !aligned4(a_zeros) || !aligned16(w_packed) ||
-      !aligned16(w_scales) || !aligned16(w_sums) || !aligned16(acc) || !aligned16(y))
+      !aligned16(w_scales) || !aligned16(w_sums) || (acc && !aligned16(acc)) || !aligned16(y))
     return DPTQ_ERR_INVALID_ARG;
   const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (decode)
+    return from_hip(dptq::launch_qlinear_zp_decode(codes, a_scales, a_zeros, M, (int)K, bits, w_packed,
+                                                   w_scales, w_sums, N, y, s));
   hipError_t e = dptq::launch_qlinear(codes, nullptr, M, (int)K, bits, w_packed, nullptr, N, nullptr,
                                       acc, dptq::kGemmAuto, s);
   if (e != hipSuccess) return from_hip(e);

@@ -824,11 +824,16 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
 constexpr int kDecWaves = 8;
 constexpr int kDecBatch = 4;
 
-template <int BITS, bool ACC_OUT>
+// ZP: the range quantizer's zero-point correction in the epilogue,
+// acc + (2^(BITS-1) - a_zeros[m]) * w_sums[n] (exact int32), before the
+// dequantization.
+template <int BITS, bool ACC_OUT, bool ZP = false>
 __global__ void __launch_bounds__(kDecWaves * 64)
 qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
              const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
-             int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
+             int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out,
+             const int32_t* __restrict__ a_zeros = nullptr,
+             const int32_t* __restrict__ w_sums = nullptr) {
   __shared__ v4i part[kDecWaves][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = blockIdx.x * 16;
@@ -885,8 +890,16 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
   }
   if (!mvalid) return;
   const int m = fr, n = n0 + fg * 4;
-  const int c0 = unscale<BITS>(tot.x), c1 = unscale<BITS>(tot.y);
-  const int c2 = unscale<BITS>(tot.z), c3 = unscale<BITS>(tot.w);
+  int c0 = unscale<BITS>(tot.x), c1 = unscale<BITS>(tot.y);
+  int c2 = unscale<BITS>(tot.z), c3 = unscale<BITS>(tot.w);
+  if constexpr (ZP) {
+    const int off = (1 << (BITS - 1)) - a_zeros[m];
+    const int4 ws = *reinterpret_cast<const int4*>(w_sums + n);
+    c0 += off * ws.x;
+    c1 += off * ws.y;
+    c2 += off * ws.z;
+    c3 += off * ws.w;
+  }
   if (ACC_OUT) {
     *reinterpret_cast<int4*>(acc_out + (size_t)m * N + n) = make_int4(c0, c1, c2, c3);
   } else {
@@ -1000,6 +1013,24 @@ bool gemm_kernel_fits(int kernel, int64_t M, int64_t N, int K, int bits) {
     default:
       return false;
   }
+}
+
+hipError_t launch_qlinear_zp_decode(const void* codes, const float* a_scales, const int32_t* a_zeros,
+                                   int64_t M, int K, int bits, const uint8_t* w_packed,
+                                   const float* w_scales, const int32_t* w_sums, int64_t N, void* y,
+                                   hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const uint8_t* a = static_cast<const uint8_t*>(codes);
+  __half* yh = static_cast<__half*>(y);
+  if (bits == 4)
+    hipLaunchKernelGGL((qgemm_decode<4, false, true>), dim3((unsigned)(N / 16)), dim3(kDecWaves * 64), 0,
+                       stream, a, a_scales, w_packed, w_scales, (int)M, (int)N, K, yh, nullptr, a_zeros,
+                       w_sums);
+  else
+    hipLaunchKernelGGL((qgemm_decode<8, false, true>), dim3((unsigned)(N / 16)), dim3(kDecWaves * 64), 0,
+                       stream, a, a_scales, w_packed, w_scales, (int)M, (int)N, K, yh, nullptr, a_zeros,
+                       w_sums);
+  return hipGetLastError();
 }
 
 hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M, int K,

@@ -300,7 +300,7 @@ def test_range_entry_points_validation(L):
     assert ql(K=200) == UNSUPPORTED
     assert ql(N=24) == UNSUPPORTED
     assert ql(bits=6) == INVALID
-    assert ql(acc=NULL) == INVALID
+    assert ql(M=17, acc=NULL) == INVALID    # prefill needs the accumulator workspace
     assert ql(sums=NULL) == INVALID
     assert ql(y=MISALIGNED) == INVALID
     assert ql(M=0, acc=NULL, y=NULL) == OK

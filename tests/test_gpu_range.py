@@ -96,9 +96,11 @@ def test_weight_sums_match_oracle(dev, N, K):
 
 
 LINEAR_CASES = [
-    # (M, K, N, h): decode GEMM (M <= 16), prefill tiles with ragged M, the
-    # tiny workload
-    (1, 4096, 512, 4096), (16, 256, 512, 256), (70, 4096, 320, 4096), (300, 1024, 256, 1024),
+    # (M, K, N, h): one launch with the correction in the decode GEMM
+    # (M <= 16), either side of that boundary, prefill tiles with ragged M,
+    # the tiny workload
+    (1, 4096, 512, 4096), (16, 256, 512, 256), (17, 512, 128, 512), (70, 4096, 320, 4096),
+    (300, 1024, 256, 1024),
     (5, 14336, 64, 28 * 512),
 ]
 
