@@ -116,10 +116,13 @@ def run_only(torch, dptq, cfg, args):
         return
     bits = 4 if args.only.endswith("4") else 8
     codes, scales = dptq.rotate_quant(x, h, bits)
+    w8 = dptq.pack_w4_a8(wp) if bits == 8 else None
     torch.cuda.synchronize()
     for _ in range(args.steps):
         if args.only.startswith("rq"):
             dptq.rotate_quant(x, h, bits, codes, scales)
+        elif bits == 8:
+            dptq.qlinear_a8(codes, scales, w8, ws, y)     # the step's A8 GEMM
         else:
             dptq.qlinear(codes, scales, bits, wp, ws, y)
     torch.cuda.synchronize()
@@ -144,6 +147,7 @@ def time_layer(torch, dptq, cfg, args):
     xs = [x.clone() for _ in range(R)]
     wps = [wp.clone() for _ in range(R)]
     w6s = [dptq.pack_fp6(wp) for _ in range(R)]      # the same weights, FP6 operand layout
+    w8s = [dptq.pack_w4_a8(wp) for _ in range(R)]    # the same weights, 8-bit activation order
     wss = [ws.clone() for _ in range(R)]
     codes8 = torch.empty((M, K), dtype=torch.int8, device=dev)
     a6 = torch.empty((dptq.fp6_bytes(M, K),), dtype=torch.uint8, device=dev)
@@ -159,7 +163,7 @@ def time_layer(torch, dptq, cfg, args):
                 dptq.qlinear_fp6(a6, scales, w6s[r], wss[r], M, K, N, y)
             else:
                 dptq.rotate_quant(xs[r], h, bits, codes8, scales)
-                dptq.qlinear(codes8, scales, bits, wps[r], wss[r], y)
+                dptq.qlinear_a8(codes8, scales, w8s[r], wss[r], y)
 
     def policy():
         bits_all = dptq.layer_policy(n_layers)
@@ -229,6 +233,7 @@ def time_kernels(torch, dptq, cfg, args, seq, reps=24):
     xs = [x.clone() for _ in range(R)]
     wps = [wp.clone() for _ in range(R)]
     w6s = [dptq.pack_fp6(wp) for _ in range(R)]
+    w8s = [dptq.pack_w4_a8(wp) for _ in range(R)]
     y = torch.empty((M, N), dtype=torch.float16, device=dev)
     out = {}
     # the step's kernels: FP6 A4 layer, int8 A8 layer
@@ -238,10 +243,16 @@ def time_kernels(torch, dptq, cfg, args, seq, reps=24):
     out["gemm_fp6_a4"] = _graph_time(torch, [
         (lambda i: (lambda: dptq.qlinear_fp6(a6, s6, w6s[i % R], ws, M, K, N, y)))(i)
         for i in range(reps)]) / 1e3
-    # the int8 matrix-core kernels for both precisions (A4 for comparison)
+    # the int8 matrix-core kernels for both precisions: the step's A8 GEMM on
+    # weights in the 8-bit activation order, and for comparison the A8 and A4
+    # GEMMs on the canonical nibble order
     for bits in (8, 4):
         codes, scales = dptq.rotate_quant(x, h, bits)
-        out[f"gemm_a{bits}"] = _graph_time(torch, [
+        if bits == 8:
+            out["gemm_a8"] = _graph_time(torch, [
+                (lambda i: (lambda: dptq.qlinear_a8(codes, scales, w8s[i % R], ws, y)))(i)
+                for i in range(reps)]) / 1e3
+        out[f"gemm_a{bits}_canonical_order"] = _graph_time(torch, [
             (lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
             for i in range(reps)]) / 1e3
         out[f"rotate_quant_a{bits}"] = _graph_time(torch, [
@@ -444,8 +455,8 @@ def time_stack(torch, dptq, name, Ms, reps=3):
     4-layer mask and all-8-bit activations, and the mixed/all-4-bit ratios.
     At prefill sizes the same policies run again with the 4-bit layers on the
     FP6 path (rotate+quantize into the FP6 layout, FP6 GEMM against weights
-    packed once into it) and the 8-bit layers on the int8 path: the "_fp6"
-    entries."""
+    packed once into it) and the 8-bit layers on the int8 path against weights
+    packed once into the 8-bit activation order: the "_fp6" entries."""
     import workloads
     dev = torch.device("cuda:0")
     cfg = workloads.CONFIGS[name]
@@ -460,9 +471,10 @@ def time_stack(torch, dptq, name, Ms, reps=3):
                 "seeded_mask": dptq.layer_policy(L, workloads.layer_mask(L, 4, cfg["mask_seed"])),
                 "all_a8": [8] * L}
     out = {"weights_GB": round(wbytes / 1e9, 2)}
-    W6 = None
+    W6 = W8 = None
     if any(M > 16 for M in Ms):
         W6 = [[dptq.pack_fp6(W[l][i][0]) for i in range(len(lins))] for l in range(L)]
+        W8 = [[dptq.pack_w4_a8(W[l][i][0]) for i in range(len(lins))] for l in range(L)]
     for M in Ms:
         X = [torch.from_numpy(workloads.stack_layer_input(name, L // 2, n, M=M)).to(dev)
              for n, *_ in lins]
@@ -505,7 +517,7 @@ def time_stack(torch, dptq, name, Ms, reps=3):
                             else:
                                 codes = cbuf[: M * K].view(torch.int8).view(M, K)
                                 dptq.rotate_quant(X[i], h, 8, codes, sbuf)
-                                dptq.qlinear(codes, sbuf, 8, W[l][i][0], W[l][i][1], y)
+                                dptq.qlinear_a8(codes, sbuf, W8[l][i], W[l][i][1], y)
                 res[pname + "_fp6"] = _graph_time(torch, [run6], reps=reps) / 1e3
             del a6buf
         ops = 2.0 * M * sum(K * N for _, K, N, _ in lins) * L
@@ -520,7 +532,7 @@ def time_stack(torch, dptq, name, Ms, reps=3):
             ent["all_a4_fp6_TOPS"] = round(ops / (res["all_a4_fp6"] * 1e-3) / 1e12, 1)
         out[f"M{M}"] = ent
         del X, cbuf, ybuf
-    del W, W6
+    del W, W6, W8
     torch.cuda.empty_cache()
     return out
 
@@ -582,7 +594,7 @@ def main():
     step_kernels = {"rotate_quant_fp6_a4": "rq_pow2_kernel<__half, 4, false, 12, false, true>",
                     "gemm_fp6_a4": "qgemm_fp6<false, false>",
                     "rotate_quant_a8": "rq_pow2_kernel<__half, 8, false, 12, false, false>",
-                    "gemm_a8": "qgemm_prefill_wide<8, false>"}
+                    "gemm_a8": "qgemm_prefill_wide<8, false, true>"}
     dominant = max(step_kernels, key=lambda k: per[k])
     dom_ms = per[dominant]
     fp6_ms = per["gemm_fp6_a4"]

@@ -145,6 +145,39 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
                         int32_t bits, const uint8_t* w_packed, const float* w_scales,
                         int64_t N, void* y, int32_t* acc, int32_t kernel, void* stream);
 
+/*
+ * dptq_pack_w4_a8 - reorders 4-bit weights for W4A8 layers (the Eq. 5 weights
+ * of the layers that Algorithm 1 step 2 / Eq. 21 run at 8 bits).  The layout is the same
+ * size as w_packed; within each 4-byte group of a row (k = 8g .. 8g+7) byte
+ * j holds k = 8g + j in its low nibble and k = 8g + j + 4 in its high nibble
+ * (4-bit two's complement).  With this order the int8 matrix cores take the
+ * 8-bit activation codes as they are stored, with no byte regrouping in the
+ * GEMM's inner loop.  Offline, once per weight matrix.
+ *
+ *   w_packed device, uint8 [N, K/2] in the dptq_qlinear layout
+ *   N        rows >= 0 (N = 0 enqueues nothing)
+ *   K        multiple of 128, 128 <= K <= DPTQ_MAX_K
+ *   out      device, uint8 [N, K/2]; must not overlap w_packed
+ */
+int dptq_pack_w4_a8(const uint8_t* w_packed, int64_t N, int64_t K, uint8_t* out, void* stream);
+
+/*
+ * dptq_qlinear_a8 - the W4A8 linear of dptq_qlinear (bits = 8) against
+ * weights in the dptq_pack_w4_a8 order: the same accumulators and outputs
+ * bit for bit.  Section 2, Eq. 5, Section 4.2.
+ *
+ *   codes    device, int8 [M, K] (dptq_rotate_quant, bits 8)
+ *   a_scales device, float [M]
+ *   w_a8     device, uint8 [N, K/2] from dptq_pack_w4_a8
+ *   w_scales device, float [N]
+ *   y        device, fp16 [M, N]
+ *   kernel   a dptq_gemm_kernel value; DPTQ_ERR_UNSUPPORTED when it does not
+ *            cover the shape; shapes and alignment as for dptq_qlinear
+ */
+int dptq_qlinear_a8(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                    const uint8_t* w_a8, const float* w_scales, int64_t N, void* y, int32_t kernel,
+                    void* stream);
+
 /* Paths of dptq_qlinear_decode_fused. */
 typedef enum {
   DPTQ_DECODE_AUTO = 0,          /* the one launch where it is the faster path */

@@ -15,7 +15,8 @@ Modules
   hadamard  Sylvester / Paley Hadamard matrices and the block rotation x.B_h
             (Section 2, Eq. 4 "rotation_activation" and Eq. 5 "rotation_equiv").
   quant     per-token / per-channel symmetric quantizer and nibble packing
-            (Section 2, Eq. 1-3; Section 4.2 quantizer facts).
+            (Section 2, Eq. 1-3; Section 4.2 quantizer facts), and the
+            weight byte order of the W4A8 GEMM.
   gemm      exact integer GEMM and the per-token x per-channel dequant epilogue
             (Section 2, Y = X W^T).
   policy    phase-aware activation bit policy (Eq. 21, Algorithm 1 step 2).
@@ -32,6 +33,7 @@ Modules
 from .hadamard import (sylvester, paley28, hadamard, split_had_size,
                        rotate_rows)
 from .quant import (qmax_for_bits, quantize_rows, pack_int4, unpack_int4,
+                    pack_int4_a8order, unpack_int4_a8order,
                     rotate_quant_ref, prepare_weights_ref, dequant_rows)
 from .gemm import qlinear_acc_ref, qlinear_acc_entries, epilogue_ref, qlinear_ref
 from .policy import layer_policy_ref
@@ -47,6 +49,7 @@ from .range_quant import (range_levels, quantize_rows_range, rotate_quant_range_
 __all__ = [
     "sylvester", "paley28", "hadamard", "split_had_size", "rotate_rows",
     "qmax_for_bits", "quantize_rows", "pack_int4", "unpack_int4",
+    "pack_int4_a8order", "unpack_int4_a8order",
     "rotate_quant_ref", "prepare_weights_ref", "dequant_rows",
     "qlinear_acc_ref", "qlinear_acc_entries", "epilogue_ref", "qlinear_ref",
     "layer_policy_ref",

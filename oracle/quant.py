@@ -27,6 +27,7 @@ import numpy as np
 from .hadamard import rotate_rows, split_had_size
 
 __all__ = ["qmax_for_bits", "quantize_rows", "pack_int4", "unpack_int4",
+           "pack_int4_a8order", "unpack_int4_a8order",
            "rotate_quant_ref", "prepare_weights_ref", "dequant_rows"]
 
 
@@ -78,6 +79,32 @@ def unpack_int4(packed):
     out[..., 0::2] = lo
     out[..., 1::2] = hi
     return out
+
+
+def pack_int4_a8order(codes):
+    """Weight codes [N, K] in [-8, 7] (K % 8 == 0) -> uint8 [N, K/2] in the
+    order the W4A8 GEMM takes: in each group of eight k (4 bytes), byte j
+    holds k = 8g + j in its low nibble and k = 8g + j + 4 in its high one.
+    A storage order only; the GEMM's result does not depend on it."""
+    c = np.asarray(codes).astype(np.int64)
+    if c.shape[-1] % 8:
+        raise ValueError("K must be a multiple of 8")
+    if c.size and (c.min() < -8 or c.max() > 7):
+        raise ValueError("int4 codes must lie in [-8, 7]")
+    g = c.reshape(c.shape[:-1] + (c.shape[-1] // 8, 8)) & 0xF
+    out = g[..., 0:4] | (g[..., 4:8] << 4)
+    return out.reshape(c.shape[:-1] + (c.shape[-1] // 2,)).astype(np.uint8)
+
+
+def unpack_int4_a8order(packed):
+    """Inverse of pack_int4_a8order: uint8 [N, K/2] -> int8 [N, K]."""
+    p = np.asarray(packed, dtype=np.uint8).astype(np.int64)
+    g = p.reshape(p.shape[:-1] + (p.shape[-1] // 4, 4))
+    lo = g & 0xF
+    hi = (g >> 4) & 0xF
+    both = np.concatenate([lo, hi], axis=-1)
+    both = np.where(both >= 8, both - 16, both)
+    return both.reshape(p.shape[:-1] + (2 * p.shape[-1],)).astype(np.int8)
 
 
 def rotate_quant_ref(x, had_size, bits):

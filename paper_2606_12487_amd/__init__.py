@@ -19,7 +19,7 @@ __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qline
            "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
            "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "DECODE_AUTO", "DECODE_ONE_LAUNCH",
            "DECODE_TWO_LAUNCHES", "rotate_quant_range", "weight_sums", "qlinear_range",
-           "qlinear_fp6_acc",
+           "qlinear_fp6_acc", "pack_w4_a8", "qlinear_a8",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
@@ -36,7 +36,8 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_fp6_bytes", "dptq_pack_fp6", "dptq_rotate_quant_fp6",
                       "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed",
                       "dptq_qlinear_decode_fused", "dptq_rotate_quant_range",
-                      "dptq_weight_sums", "dptq_qlinear_range")
+                      "dptq_weight_sums", "dptq_qlinear_range", "dptq_pack_w4_a8",
+                      "dptq_qlinear_a8")
 
 # Code layouts of dptq_rotate_quant_ex.
 LAYOUT_PACKED, LAYOUT_FP6 = 0, 1
@@ -112,6 +113,10 @@ def lib():
         L.dptq_qlinear_range.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
+        L.dptq_pack_w4_a8.argtypes = [vp, i64, i64, vp, vp]
+        L.dptq_pack_w4_a8.restype = ctypes.c_int
+        L.dptq_qlinear_a8.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, i32, vp]
+        L.dptq_qlinear_a8.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -251,6 +256,37 @@ def qlinear_acc(codes, bits, w_packed, acc=None, kernel=GEMM_AUTO):
                                          N, None, _ptr(acc), int(kernel), _stream(codes)),
                "dptq_qlinear_kernel")
     return acc
+
+
+def pack_w4_a8(w_packed, out=None):
+    """4-bit weights [N, K/2] in the qlinear layout -> the same codes in the
+    8-bit activation order (uint8 [N, K/2]) taken by qlinear_a8."""
+    torch = _torch()
+    _require(w_packed, "w_packed", torch.uint8)
+    if w_packed.dim() != 2:
+        raise ValueError("w_packed must be 2-D [N, K/2]")
+    N, K = w_packed.shape[0], w_packed.shape[1] * 2
+    if out is None:
+        out = torch.empty_like(w_packed)
+    _require(out, "out", torch.uint8, (N, K // 2))
+    _check(lib().dptq_pack_w4_a8(_ptr(w_packed), N, K, _ptr(out), _stream(w_packed)),
+           "dptq_pack_w4_a8")
+    return out
+
+
+def qlinear_a8(codes, a_scales, w_a8, w_scales, y=None, kernel=GEMM_AUTO):
+    """The W4A8 linear (qlinear with bits = 8) against weights from pack_w4_a8:
+    the same y bit for bit."""
+    torch = _torch()
+    M, K, N = _gemm_args(codes, 8, w_a8)
+    _require(a_scales, "a_scales", torch.float32, (M,))
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
+    _require(y, "y", torch.float16, (M, N))
+    _check(lib().dptq_qlinear_a8(_ptr(codes), _ptr(a_scales), M, K, _ptr(w_a8), _ptr(w_scales), N,
+                                 _ptr(y), int(kernel), _stream(codes)), "dptq_qlinear_a8")
+    return y
 
 
 def residual_dynamics(x, dx, had_size, bits=4, eps=1e-8, jr=None, snr=None, means=None):

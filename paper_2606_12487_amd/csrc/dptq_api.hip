@@ -189,6 +189,31 @@ int dptq_qlinear_kernel(const void* codes, const float* a_scales, int64_t M, int
                                        nullptr, acc, kernel, static_cast<hipStream_t>(stream)));
 }
 
+int dptq_pack_w4_a8(const uint8_t* w_packed, int64_t N, int64_t K, uint8_t* out, void* stream) {
+  if (N < 0 || K < 1) return DPTQ_ERR_INVALID_ARG;
+  if (K % 128 != 0 || K > DPTQ_MAX_K || N > 0x7FFFFFF0) return DPTQ_ERR_UNSUPPORTED;
+  if (N == 0) return DPTQ_OK;
+  if (!w_packed || !out) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(w_packed) || !aligned16(out)) return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_pack_w4_a8(w_packed, N, (int)K, out, static_cast<hipStream_t>(stream)));
+}
+
+int dptq_qlinear_a8(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                    const uint8_t* w_a8, const float* w_scales, int64_t N, void* y, int32_t kernel,
+                    void* stream) {
+  int st = check_gemm_shape(M, K, 8, N);
+  if (st != DPTQ_OK) return st;
+  if (kernel < DPTQ_GEMM_AUTO || kernel > DPTQ_GEMM_TILE_192X256) return DPTQ_ERR_INVALID_ARG;
+  if (!dptq::gemm_kernel_fits(kernel, M, N, (int)K, 8)) return DPTQ_ERR_UNSUPPORTED;
+  if (M == 0) return DPTQ_OK;
+  if (!codes || !a_scales || !w_a8 || !w_scales || !y) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(a_scales) || !aligned16(w_a8) || !aligned16(w_scales) ||
+      !aligned16(y))
+    return DPTQ_ERR_INVALID_ARG;
+  return from_hip(dptq::launch_qlinear_a8(codes, a_scales, M, (int)K, w_a8, w_scales, N, y, kernel,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 int64_t dptq_fp6_bytes(int64_t rows, int64_t K) {
   if (rows < 0 || K < 128 || K % 128 != 0 || K > DPTQ_MAX_K || rows > 0x7FFFFFFF) return -1;
   return dptq::fp6_bytes(rows, K);

@@ -59,6 +59,17 @@ hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
                           const float* w_scales, int64_t N, void* y,
                           int32_t* out_acc, int kernel, hipStream_t stream);
 
+// 4-bit weights [N, K/2] in the canonical nibble order -> the 8-bit
+// activation order (per dword: k0..k3 in the low nibbles, k4..k7 in the high
+// ones; K % 8 == 0).
+hipError_t launch_pack_w4_a8(const uint8_t* w_packed, int64_t N, int K, uint8_t* out,
+                             hipStream_t stream);
+// W4A8 GEMM + epilogue against weights in the 8-bit activation order; the
+// kernel choice as for launch_qlinear.
+hipError_t launch_qlinear_a8(const void* codes, const float* a_scales, int64_t M, int K,
+                             const uint8_t* w_a8, const float* w_scales, int64_t N, void* y,
+                             int kernel, hipStream_t stream);
+
 // Dynamic LDS available to the fused decode kernel (160 KiB less its 8.1 KiB
 // of static arrays, rounded down).
 constexpr int64_t kFusedLdsMax = 151 * 1024;

@@ -18,6 +18,9 @@
 // B operand the activation tile (columns = tokens m).  Each lane then holds
 // four consecutive n of one m, i.e. 8 contiguous bytes of a row of y.
 
+#include <utility>
+
+#include "dptq.h"
 #include "internal.h"
 
 namespace dptq {
@@ -55,6 +58,26 @@ __device__ __forceinline__ v4i op_from_bytes(uint32_t d0, uint32_t d1, uint32_t 
   r.z = (int)even_bytes(d2, d3);
   r.w = (int)odd_bytes(d2, d3);
   return r;
+}
+
+// 8-bit activation operand of one 32-k step.  Against weights in the
+// canonical nibble order the activation bytes are regrouped like the nibble
+// unpack (even k, then odd k).  Weights in the 8-bit order (each dword holds
+// k0..k3 in its low nibbles and k4..k7 in its high ones, pack_w4_a8_kernel)
+// unpack to natural k order, so the activation dwords are the operand as
+// they stand.
+template <bool WA8>
+__device__ __forceinline__ v4i op_a8(uint32_t d0, uint32_t d1, uint32_t d2, uint32_t d3) {
+  if constexpr (WA8) {
+    v4i r;
+    r.x = (int)d0;
+    r.y = (int)d1;
+    r.z = (int)d2;
+    r.w = (int)d3;
+    return r;
+  } else {
+    return op_from_bytes(d0, d1, d2, d3);
+  }
 }
 
 __device__ __forceinline__ v4i mfma(v4i a, v4i b, v4i c) {
@@ -103,6 +126,17 @@ __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t
                :
                : "v"(voff), "s"(sbase), "s"(lds_off)
                : "memory", "m0");
+}
+
+// The same with the LDS destination given as a wavefront-uniform base plus a
+// compile-time offset, formed in M0 by one scalar add (the global address is
+// sbase + voff, the per-lane offset carrying the row).
+template <uint32_t OFF>
+__device__ __forceinline__ void dma16_at(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_base), "i"(OFF)
+               : "memory", "m0", "scc");
 }
 
 // The same with 4 bytes per lane (LDS byte offset lds_off + 4 * lane).
@@ -168,7 +202,7 @@ struct Cfg {
 
 template <int BITS> using PrefillCfg = Cfg<BITS, 256, 128, 4, 2>;
 
-template <class C, bool ACC_OUT>
+template <class C, bool ACC_OUT, bool WA8 = false>
 __global__ void __launch_bounds__(C::kThreads)
 qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
               const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
@@ -338,7 +372,7 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
 #pragma unroll
       for (int j = 0; j < kTJ; ++j) {
         if (BITS == 4) aop[j] = op_from_nibbles(f.a[j][2 * kk], f.a[j][2 * kk + 1]);
-        else aop[j] = op_from_bytes(f.a[j][4 * kk], f.a[j][4 * kk + 1], f.a[j][4 * kk + 2], f.a[j][4 * kk + 3]);
+        else aop[j] = op_a8<WA8>(f.a[j][4 * kk], f.a[j][4 * kk + 1], f.a[j][4 * kk + 2], f.a[j][4 * kk + 3]);
       }
 #pragma unroll
       for (int i = 0; i < kTI; ++i) {
@@ -540,7 +574,7 @@ __device__ __forceinline__ uint2 dequant4(int a0, int a1, int a2, int a3, float 
   return pk;
 }
 
-template <int BITS, bool ACC_OUT>
+template <int BITS, bool ACC_OUT, bool WA8 = false>
 __global__ void __launch_bounds__(256)
 qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
                    const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
@@ -583,18 +617,31 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
   const uint32_t alane =
       BITS == 4 ? (uint32_t)((lane >> 2) * arow + (((lane & 3) ^ ((lane >> 4) & 3)) * 16))
                 : (uint32_t)((lane >> 3) * arow + (((lane & 7) ^ ((4 * (wave & 1) + (lane >> 4)) & 7)) * 16));
+  // The row part of each load's address is loop-invariant and lives in the
+  // per-lane offset (below 2^32: 256 rows of at most DPTQ_MAX_K bytes), so one
+  // stage's loads share one scalar base per operand and each costs a single
+  // scalar add (its M0).
+  static_assert((uint64_t)C::kBM * DPTQ_MAX_K < (1ull << 32), "32-bit load offsets");
+  uint32_t wofs[C::kWLoads], aofs[C::kALoads];
+#pragma unroll
+  for (int i = 0; i < C::kWLoads; ++i) wofs[i] = wlane + (uint32_t)((4 * i + wave) * 16) * (uint32_t)wrow;
+#pragma unroll
+  for (int i = 0; i < C::kALoads; ++i) aofs[i] = alane + (uint32_t)((4 * i + wave) * kARows) * (uint32_t)arow;
   const uint32_t smem_base = (uint32_t)(uintptr_t)(lds_ptr)smem;
-  auto issue = [&](int m0, int n0, int st, int buf) __attribute__((always_inline)) {
+  // wtile, atile: the tile's first weight and activation rows (uniform).
+  auto issue = [&](const uint8_t* wtile, const uint8_t* atile, int st, int buf) __attribute__((always_inline)) {
     const uint32_t base = smem_base + buf * C::kStage + wave * 1024;
-    const uint8_t* wt = w_packed + (size_t)n0 * wrow + (size_t)st * C::kWRow;   // uniform
-    const uint8_t* at = a_codes + (size_t)m0 * arow + (size_t)st * C::kARow;    // uniform
-#pragma unroll
-    for (int i = 0; i < C::kWLoads; ++i)
-      dma16(wt + (size_t)((4 * i + wave) * 16) * wrow, wlane, base + i * 4096);
-#pragma unroll
-    for (int i = 0; i < C::kALoads; ++i)
-      dma16(at + (size_t)((4 * i + wave) * kARows) * arow, alane, base + C::kW + i * 4096);
+    const uint8_t* wt = wtile + (size_t)st * C::kWRow;
+    const uint8_t* at = atile + (size_t)st * C::kARow;
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      (dma16_at<(uint32_t)(I * 4096)>(wt, wofs[I], base), ...);
+    }(std::make_integer_sequence<int, C::kWLoads>{});
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      (dma16_at<(uint32_t)(C::kW + I * 4096)>(at, aofs[I], base), ...);
+    }(std::make_integer_sequence<int, C::kALoads>{});
   };
+  auto wtile_of = [&](int n0) __attribute__((always_inline)) { return w_packed + (size_t)n0 * wrow; };
+  auto atile_of = [&](int m0) __attribute__((always_inline)) { return a_codes + (size_t)m0 * arow; };
   // Scales of a tile into slot q (only when producing y; the accumulator
   // output has none): wavefront 0 loads a_s [256] in four 4-byte-per-lane
   // loads (a shifted tile's m0 need not be 16-byte aligned), wavefront 1
@@ -666,7 +713,7 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
 #pragma unroll
     for (int j = 0; j < kTJ; ++j) {
       if (BITS == 4) o.a[j] = op_from_nibbles(p.a[j][2 * kk], p.a[j][2 * kk + 1]);
-      else o.a[j] = op_from_bytes(p.a[j][4 * kk], p.a[j][4 * kk + 1], p.a[j][4 * kk + 2], p.a[j][4 * kk + 3]);
+      else o.a[j] = op_a8<WA8>(p.a[j][4 * kk], p.a[j][4 * kk + 1], p.a[j][4 * kk + 2], p.a[j][4 * kk + 3]);
     }
   };
   v16i acc[kTI][kTJ];
@@ -742,11 +789,13 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
   int m0, n0;
   origin(0, m0, n0);
   issue_scales(m0, n0, 0);
+  const uint8_t* wt0 = wtile_of(n0);
+  const uint8_t* at0 = atile_of(m0);
 #pragma unroll
-  for (int st = 0; st < kB - 1; ++st) issue(m0, n0, st, st);
+  for (int st = 0; st < kB - 1; ++st) issue(wt0, at0, st, st);
   wait_vmcnt<(kB - 2) * C::kLoads>();
   lds_barrier();
-  issue(m0, n0, kB - 1, kB - 1);
+  issue(wt0, at0, kB - 1, kB - 1);
   read_chunk(0, 0, p0);
   unpack(p0, 0, u0);
   int cur = 0;   // buffer of the current stage
@@ -754,6 +803,8 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
     const bool has_next = r + 1 < ntile;
     int m1 = m0, n1 = n0;
     if (has_next) origin(r + 1, m1, n1);
+    const uint8_t* wt1 = wtile_of(n1);
+    const uint8_t* at1 = atile_of(m1);
 #pragma unroll
     for (int i = 0; i < kTI; ++i)
 #pragma unroll
@@ -773,7 +824,7 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
       // this tile's last stage again).
       const int si = s + kB;
       const bool in_next = si >= nst;
-      issue(in_next ? m1 : m0, in_next ? n1 : n0, in_next ? (has_next ? si - nst : nst - 1) : si, cur);
+      issue(in_next ? wt1 : wt0, in_next ? at1 : at0, in_next ? (has_next ? si - nst : nst - 1) : si, cur);
       read_chunk(nxt, 0, p0);
       mfmas(u0);
       unpack(p1, 1, u1);
@@ -796,7 +847,7 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
       if (has_next) {
         wait_vmcnt<(kB - 2) * C::kLoads>();
         lds_barrier();
-        issue(m1, n1, kB - 1, cur);
+        issue(wt1, at1, kB - 1, cur);
         issue_scales(m1, n1, (r + 1) & 1);
       }
       mfmas(u0);
@@ -812,6 +863,8 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
     }
     m0 = m1;
     n0 = n1;
+    wt0 = wt1;
+    at0 = at1;
   }
   wait_vmcnt<0>();   // the re-issued tail loads land before the workgroup's LDS is released
 }
@@ -827,7 +880,7 @@ constexpr int kDecBatch = 4;
 // ZP: the range quantizer's zero-point correction in the epilogue,
 // acc + (2^(BITS-1) - a_zeros[m]) * w_sums[n] (exact int32), before the
 // dequantization.
-template <int BITS, bool ACC_OUT, bool ZP = false>
+template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false>
 __global__ void __launch_bounds__(kDecWaves * 64)
 qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
              const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
@@ -872,8 +925,8 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
         b0 = op_from_nibbles(av[b].x, av[b].y);
         b1 = op_from_nibbles(av[b].z, av[b].w);
       } else {
-        b0 = op_from_bytes(av[b].x, av[b].y, av[b].z, av[b].w);
-        b1 = op_from_bytes(av2[b].x, av2[b].y, av2[b].z, av2[b].w);
+        b0 = op_a8<WA8>(av[b].x, av[b].y, av[b].z, av[b].w);
+        b1 = op_a8<WA8>(av2[b].x, av2[b].y, av2[b].z, av2[b].w);
       }
       acc = mfma(op_from_nibbles(wv[b].x, wv[b].y), b0, acc);
       acc = mfma(op_from_nibbles(wv[b].z, wv[b].w), b1, acc);
@@ -914,21 +967,39 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
   }
 }
 
-template <class C, bool ACC_OUT>
+// Weights in the 8-bit activation order: dword g of a row holds k = 8g ..
+// 8g + 7; canonical nibble i (bits 4i..4i+3) is k = 8g + i, and the packed
+// byte j holds k = 8g + j in its low nibble and k = 8g + j + 4 in its high
+// one.  One dword per thread.
+__global__ void __launch_bounds__(256)
+pack_w4_a8_kernel(const uint32_t* __restrict__ w, int64_t ndw, uint32_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= ndw) return;
+  const uint32_t v = w[i];
+  uint32_t o = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    o |= ((v >> (4 * j)) & 0xFu) << (8 * j);
+    o |= ((v >> (4 * (j + 4))) & 0xFu) << (8 * j + 4);
+  }
+  out[i] = o;
+}
+
+template <class C, bool ACC_OUT, bool WA8 = false>
 void launch_prefill(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
                     const float* ws, int64_t N, __half* y, int32_t* acc, hipStream_t stream) {
   const int64_t tiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
-  hipLaunchKernelGGL((qgemm_prefill<C, ACC_OUT>), dim3((unsigned)tiles), dim3(C::kThreads), 0,
+  hipLaunchKernelGGL((qgemm_prefill<C, ACC_OUT, WA8>), dim3((unsigned)tiles), dim3(C::kThreads), 0,
                      stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
 }
 
-template <int BITS, bool ACC_OUT>
+template <int BITS, bool ACC_OUT, bool WA8 = false>
 void launch_wide(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
                  const float* ws, int64_t N, __half* y, int32_t* acc, int cus, hipStream_t stream) {
   using C = Wide<BITS>;
   const int64_t tiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
   const int64_t grid = tiles < cus ? tiles : cus;
-  hipLaunchKernelGGL((qgemm_prefill_wide<BITS, ACC_OUT>), dim3((unsigned)grid), dim3(C::kThreads), 0,
+  hipLaunchKernelGGL((qgemm_prefill_wide<BITS, ACC_OUT, WA8>), dim3((unsigned)grid), dim3(C::kThreads), 0,
                      stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
 }
 
@@ -964,7 +1035,7 @@ int auto_kernel(int64_t M, int64_t N, int K) {
   return kGemmTile;
 }
 
-template <int BITS, bool ACC_OUT>
+template <int BITS, bool ACC_OUT, bool WA8 = false>
 hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
                     const uint8_t* w, const float* ws, int64_t N, __half* y,
                     int32_t* acc, int kernel, hipStream_t stream) {
@@ -972,14 +1043,14 @@ hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
   if (kernel == kGemmAuto) kernel = auto_kernel<BITS>(M, N, K);
   switch (kernel) {
     case kGemmDecode:
-      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT>), dim3((unsigned)(N / 16)),
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, false, WA8>), dim3((unsigned)(N / 16)),
                          dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
       break;
     case kGemmWide:
-      launch_wide<BITS, ACC_OUT>(a, as, M, K, w, ws, N, y, acc, device_cus(), stream);
+      launch_wide<BITS, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, device_cus(), stream);
       break;
     default:
-      launch_prefill<PrefillCfg<BITS>, ACC_OUT>(a, as, M, K, w, ws, N, y, acc, stream);
+      launch_prefill<PrefillCfg<BITS>, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, stream);
       break;
   }
   return hipGetLastError();
@@ -1046,6 +1117,22 @@ hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M, i
   if (bits == 4)
     return launch_t<4, false>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr, kernel, stream);
   return launch_t<8, false>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr, kernel, stream);
+}
+
+hipError_t launch_pack_w4_a8(const uint8_t* w_packed, int64_t N, int K, uint8_t* out,
+                             hipStream_t stream) {
+  const int64_t ndw = N * (K / 8);
+  if (ndw == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_w4_a8_kernel, dim3((unsigned)((ndw + 255) / 256)), dim3(256), 0, stream,
+                     reinterpret_cast<const uint32_t*>(w_packed), ndw, reinterpret_cast<uint32_t*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_qlinear_a8(const void* codes, const float* a_scales, int64_t M, int K,
+                             const uint8_t* w_a8, const float* w_scales, int64_t N, void* y,
+                             int kernel, hipStream_t stream) {
+  return launch_t<8, false, true>(static_cast<const uint8_t*>(codes), a_scales, M, K, w_a8, w_scales,
+                                  N, static_cast<__half*>(y), nullptr, kernel, stream);
 }
 
 }  // namespace dptq

@@ -257,6 +257,27 @@ def test_fp6_entry_points_validation(L):
     assert L.dptq_rotate_quant_fp6(FAKE, 4, 192, 64, FAKE, FAKE, NULL) == UNSUPPORTED
 
 
+def test_a8order_entry_points_validation(L):
+    pk = L.dptq_pack_w4_a8
+    assert pk(FAKE, -1, 256, FAKE, NULL) == INVALID
+    assert pk(FAKE, 4, 192, FAKE, NULL) == UNSUPPORTED
+    assert pk(FAKE, 4, 256, MISALIGNED, NULL) == INVALID
+    assert pk(NULL, 4, 256, FAKE, NULL) == INVALID
+    assert pk(NULL, 0, 256, NULL, NULL) == OK
+
+    def qa(codes=FAKE, a_s=FAKE, M=300, K=1024, w=FAKE, w_s=FAKE, N=272, y=FAKE, kernel=0):
+        return L.dptq_qlinear_a8(codes, a_s, M, K, w, w_s, N, y, kernel, NULL)
+    assert qa(kernel=4) == INVALID
+    assert qa(kernel=dptq.GEMM_DECODE) == UNSUPPORTED          # M > 16
+    assert qa(kernel=dptq.GEMM_TILE_192X256, M=255) == UNSUPPORTED
+    assert qa(K=200) == UNSUPPORTED
+    assert qa(N=24) == UNSUPPORTED
+    for name in ("codes", "a_s", "w", "w_s", "y"):
+        assert qa(**{name: NULL}) == INVALID, name
+        assert qa(**{name: MISALIGNED}) == INVALID, name
+    assert qa(M=0, codes=NULL, a_s=NULL, w=NULL, w_s=NULL, y=NULL) == OK
+
+
 def test_fused_decode_validation(L):
     def call(M=4, K=4096, h=4096, bits=4, N=64, x=FAKE, y=FAKE, codes=FAKE, scales=FAKE, mode=1):
         return L.dptq_qlinear_decode_fused(x, M, K, h, bits, FAKE, FAKE, N, y, codes, scales, mode,

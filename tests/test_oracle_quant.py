@@ -242,3 +242,36 @@ def test_near_tie_quotients_match_exact_rational(bits):
         bc, bs = _brute_force_quantize(y[m], bits)
         assert float(scales[m]) == bs
         assert codes[m].tolist() == bc
+
+
+# --------------------------------------------------------------------------
+# the weight byte order of the W4A8 GEMM (a storage order: same codes)
+# --------------------------------------------------------------------------
+def test_a8order_worked_examples():
+    from oracle import pack_int4_a8order, unpack_int4_a8order
+    # k = 0..7 -> byte j = k_j | k_{j+4} << 4, worked by hand.
+    assert pack_int4_a8order(np.arange(8)[None, :]).tolist() == [[0x40, 0x51, 0x62, 0x73]]
+    # Negative codes are 4-bit two's complement: -8 -> 8, -1 -> 15, -2 -> 14.
+    c = np.array([[-8, -1, 7, -2, 1, -8, 0, 3]])
+    assert pack_int4_a8order(c).tolist() == [[0x18, 0x8F, 0x07, 0x3E]]
+    assert unpack_int4_a8order(np.array([[0x18, 0x8F, 0x07, 0x3E]], np.uint8)).tolist() == c.tolist()
+
+
+def test_a8order_round_trip_and_gemm_invariance():
+    from oracle import pack_int4_a8order, unpack_int4_a8order
+    rng = np.random.default_rng(41)
+    w = rng.integers(-8, 8, size=(6, 256))
+    p = pack_int4_a8order(w)
+    assert p.shape == (6, 128) and p.dtype == np.uint8
+    assert np.array_equal(unpack_int4_a8order(p), w)
+    # Relative to the canonical packing, only the nibbles inside each 4-byte
+    # group move: the multiset of nibbles per group is unchanged.
+    canon = pack_int4(w)
+    for g in range(0, 128, 4):
+        a = sorted([b & 15 for b in canon[0, g:g + 4]] + [b >> 4 for b in canon[0, g:g + 4]])
+        b = sorted([x & 15 for x in p[0, g:g + 4]] + [x >> 4 for x in p[0, g:g + 4]])
+        assert a == b
+    # A dot product read through either order is the same integer.
+    a8 = rng.integers(-128, 128, size=256)
+    assert int(np.dot(a8, unpack_int4_a8order(p)[2].astype(np.int64))) == \
+        sum(int(a8[k]) * int(w[2, k]) for k in range(256))
