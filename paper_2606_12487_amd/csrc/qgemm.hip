@@ -870,9 +870,11 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Decode (M <= 16): one workgroup per 16 output channels; its 8 wavefronts
-// split K, stream the weight rows once with 16-byte loads, and the int32
-// partial tiles are summed exactly in LDS.
+// Decode (M <= 16): one workgroup per NB blocks of 16 output channels; its 8
+// wavefronts split K, stream the weight rows once with 16-byte loads, and
+// the int32 partial tiles are summed exactly in LDS.  Every workgroup reads
+// all M activation rows of its K range, so when those rows are as many bytes
+// as its weights two blocks share them (NB = 2).
 // ---------------------------------------------------------------------------
 constexpr int kDecWaves = 8;
 constexpr int kDecBatch = 4;
@@ -880,34 +882,41 @@ constexpr int kDecBatch = 4;
 // ZP: the range quantizer's zero-point correction in the epilogue,
 // acc + (2^(BITS-1) - a_zeros[m]) * w_sums[n] (exact int32), before the
 // dequantization.
-template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false>
+template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false, int NB = 1>
 __global__ void __launch_bounds__(kDecWaves * 64)
 qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
              const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
              int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out,
              const int32_t* __restrict__ a_zeros = nullptr,
              const int32_t* __restrict__ w_sums = nullptr) {
-  __shared__ v4i part[kDecWaves][64];
+  static_assert(NB == 1 || NB == 2, "blocks per workgroup");
+  __shared__ v4i part[NB][kDecWaves][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n0 = blockIdx.x * 16;
+  const int n0 = blockIdx.x * 16 * NB;
   const int fr = lane & 15, fg = lane >> 4;
   const int nck = K / 128;
   const int c_begin = (int)((long)nck * wave / kDecWaves);
   const int c_end = (int)((long)nck * (wave + 1) / kDecWaves);
   const bool mvalid = fr < M;
 
-  const uint8_t* wp = w_packed + (size_t)(n0 + fr) * (K / 2) + fg * 16;
+  const size_t wrow = (size_t)K / 2;
+  const uint8_t* wp = w_packed + (size_t)(n0 + fr) * wrow + fg * 16;
   const size_t arow = BITS == 4 ? (size_t)K / 2 : (size_t)K;
   const uint8_t* ap = a_codes + (size_t)(mvalid ? fr : 0) * arow + (BITS == 4 ? fg * 16 : fg * 32);
 
-  v4i acc = v4i{0, 0, 0, 0};
+  v4i acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = v4i{0, 0, 0, 0};
   for (int c = c_begin; c < c_end; c += kDecBatch) {
-    uint4 wv[kDecBatch], av[kDecBatch], av2[kDecBatch];
+    uint4 wv[NB][kDecBatch], av[kDecBatch], av2[kDecBatch];
 #pragma unroll
     for (int b = 0; b < kDecBatch; ++b) {
       const int ck = c + b;
       const bool ok = ck < c_end;
-      wv[b] = ok ? *reinterpret_cast<const uint4*>(wp + (size_t)ck * 64) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        wv[nb][b] = ok ? *reinterpret_cast<const uint4*>(wp + (size_t)nb * 16 * wrow + (size_t)ck * 64)
+                       : make_uint4(0, 0, 0, 0);
       if (BITS == 4) {
         av[b] = (ok && mvalid) ? *reinterpret_cast<const uint4*>(ap + (size_t)ck * 64)
                                : make_uint4(0, 0, 0, 0);
@@ -928,21 +937,26 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
         b0 = op_a8<WA8>(av[b].x, av[b].y, av[b].z, av[b].w);
         b1 = op_a8<WA8>(av2[b].x, av2[b].y, av2[b].z, av2[b].w);
       }
-      acc = mfma(op_from_nibbles(wv[b].x, wv[b].y), b0, acc);
-      acc = mfma(op_from_nibbles(wv[b].z, wv[b].w), b1, acc);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        acc[nb] = mfma(op_from_nibbles(wv[nb][b].x, wv[nb][b].y), b0, acc[nb]);
+        acc[nb] = mfma(op_from_nibbles(wv[nb][b].z, wv[nb][b].w), b1, acc[nb]);
+      }
     }
   }
-  part[wave][lane] = acc;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) part[nb][wave][lane] = acc[nb];
   __syncthreads();
-  if (wave != 0) return;
-  v4i tot = part[0][lane];
+  // Wavefront nb < NB sums and writes block nb.
+  if (wave >= NB) return;
+  v4i tot = part[wave][0][lane];
 #pragma unroll
   for (int w = 1; w < kDecWaves; ++w) {
-    const v4i p = part[w][lane];
+    const v4i p = part[wave][w][lane];
     tot.x += p.x; tot.y += p.y; tot.z += p.z; tot.w += p.w;
   }
   if (!mvalid) return;
-  const int m = fr, n = n0 + fg * 4;
+  const int m = fr, n = n0 + wave * 16 + fg * 4;
   int c0 = unscale<BITS>(tot.x), c1 = unscale<BITS>(tot.y);
   int c2 = unscale<BITS>(tot.z), c3 = unscale<BITS>(tot.w);
   if constexpr (ZP) {
@@ -964,6 +978,33 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
     pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
     pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
     *reinterpret_cast<uint2*>(y + (size_t)m * N + n) = pk;
+  }
+}
+
+// Blocks of 16 output channels per decode workgroup.  A one-block workgroup
+// reads M * K * bits / 8 activation bytes beside 8 K weight bytes; once the
+// activations are as large (M * bits >= 64) two blocks share them, provided
+// N still gives two workgroups per compute unit.  (Four blocks were slower
+// at 8 tokens and 4 bits on the 57344-channel shape: measured.)
+int decode_blocks(int64_t M, int64_t N, int bits, int cus) {
+  if (M * bits >= 64 && N % 32 == 0 && N / 32 >= 2 * (int64_t)cus) return 2;
+  return 1;
+}
+
+template <int BITS, bool ACC_OUT, bool WA8>
+void launch_decode(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
+                   const float* ws, int64_t N, __half* y, int32_t* acc, hipStream_t stream) {
+  switch (decode_blocks(M, N, BITS, device_cus())) {
+    case 2:
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, false, WA8, 2>), dim3((unsigned)(N / 32)),
+                         dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
+                         nullptr, nullptr);
+      break;
+    default:
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, false, WA8, 1>), dim3((unsigned)(N / 16)),
+                         dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
+                         nullptr, nullptr);
+      break;
   }
 }
 
@@ -1043,8 +1084,7 @@ hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
   if (kernel == kGemmAuto) kernel = auto_kernel<BITS>(M, N, K);
   switch (kernel) {
     case kGemmDecode:
-      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, false, WA8>), dim3((unsigned)(N / 16)),
-                         dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+      launch_decode<BITS, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, stream);
       break;
     case kGemmWide:
       launch_wide<BITS, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, device_cus(), stream);

@@ -66,6 +66,8 @@ CASES = [
     # tiles with shifted edge tiles, several tiles per compute unit
     (1, 128, 16), (5, 1024, 48), (16, 4096, 272), (17, 256, 32), (130, 1024, 400),
     (256, 512, 192), (300, 640, 208), (511, 1024, 400), (1024, 4096, 2048),
+    # decode workgroups of two blocks of 16 channels
+    (8, 512, 32768), (12, 256, 16384),
 ]
 
 

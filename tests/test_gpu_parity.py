@@ -230,6 +230,10 @@ GEMM_CASES = [
     (256, 512, 192, None), (511, 640, 400, None),
     (2048, 4096, 12288, 48), (2048, 14336, 4096, 32), (4096, 8192, 1024, 32),
     (2100, 1024, 12304, 48),
+    # decode workgroups of two blocks of 16 channels (wide N, M * bits >= 64:
+    # both widths at 16 tokens, A8 at 8) and of one block just below that
+    (4, 256, 32768, None), (16, 128, 57344, None), (8, 1024, 16384, None), (7, 384, 24576, None),
+    (3, 512, 32768, None),
 ]
 
 # Every kernel must return the same bits; each case runs the automatic
