@@ -360,9 +360,9 @@ def time_decode_fused(torch, dptq):
 
 def time_range(torch, dptq, cfg):
     """The range quantizer variant (Eq. 1 with a zero point) at the step's
-    shape, next to the symmetric path: rotate + quantize, and the linear
-    (GEMM into the accumulator plus the zero-point epilogue), each timed over
-    24 graph-replayed launches."""
+    shape, next to the symmetric path: rotate + quantize, and the linear (the
+    zero-point correction in the GEMM epilogue), each timed over 24
+    graph-replayed launches."""
     import numpy as np
     import workloads
     dev = torch.device("cuda:0")
@@ -373,7 +373,6 @@ def time_range(torch, dptq, cfg):
     ws = torch.from_numpy(workloads.random_scales(rng, N)).to(dev)
     sums = dptq.weight_sums(wp)
     y = torch.empty((M, N), dtype=torch.float16, device=dev)
-    acc = torch.empty((M, N), dtype=torch.int32, device=dev)
     out = {"weight_sums_us": round(_graph_time(torch, [lambda: dptq.weight_sums(wp, sums)] * 24), 2)}
     for bits in (4, 8):
         c, s = dptq.rotate_quant(x, h, bits)
@@ -384,7 +383,7 @@ def time_range(torch, dptq, cfg):
                 torch, [lambda: dptq.rotate_quant_range(x, h, bits, cr, sr, zr)] * 24), 2),
             "qlinear_us": round(_graph_time(torch, [lambda: dptq.qlinear(c, s, bits, wp, ws, y)] * 24), 2),
             "qlinear_range_us": round(_graph_time(
-                torch, [lambda: dptq.qlinear_range(cr, sr, zr, bits, wp, ws, sums, y, acc)] * 24), 2),
+                torch, [lambda: dptq.qlinear_range(cr, sr, zr, bits, wp, ws, sums, y)] * 24), 2),
         }
     return out
 

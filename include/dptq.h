@@ -260,21 +260,18 @@ int dptq_weight_sums(const uint8_t* w_packed, int64_t N, int64_t K, int32_t* w_s
  *             = sum_k (q[m, k] - a_zeros[m]) w[n, k]            (exact int32)
  *   y[m, n]    = fl16(fl32(fl32(fl32(acc'[m, n]) * a_scales[m]) * w_scales[n]))
  *
- * M <= 16: one launch, the decode GEMM with the correction in its epilogue.
- * M > 16: two launches, dptq_qlinear_acc's GEMM into acc, then the correction
- * and the epilogue.
+ * One launch on the kernel dptq_qlinear chooses for the shape, the
+ * correction applied in the GEMM's epilogue; no workspace.
  *
  *   codes, a_scales, a_zeros  dptq_rotate_quant_range's outputs for M rows
+ *                             (a_scales 16-byte aligned, a_zeros 4-byte)
  *   M, K, bits, w_packed, w_scales, N   as for dptq_qlinear
  *   w_sums    device, int32 [N] (dptq_weight_sums), 16-byte aligned
- *   acc       device, int32 [M, N] workspace, 16-byte aligned; holds the
- *             uncorrected accumulator afterwards when M > 16; may be NULL (and
- *             is untouched) when M <= 16
  *   y         device, fp16 [M, N] output, 16-byte aligned
  */
 int dptq_qlinear_range(const void* codes, const float* a_scales, const int32_t* a_zeros, int64_t M,
                        int64_t K, int32_t bits, const uint8_t* w_packed, const float* w_scales,
-                       const int32_t* w_sums, int64_t N, int32_t* acc, void* y, void* stream);
+                       const int32_t* w_sums, int64_t N, void* y, void* stream);
 
 /*
  * dptq_residual_dynamics - residual-dynamics calibration statistics of one

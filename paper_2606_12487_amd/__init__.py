@@ -109,7 +109,7 @@ def lib():
         L.dptq_rotate_quant_range.restype = ctypes.c_int
         L.dptq_weight_sums.argtypes = [vp, i64, i64, vp, vp]
         L.dptq_weight_sums.restype = ctypes.c_int
-        L.dptq_qlinear_range.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp, i64, vp, vp, vp]
+        L.dptq_qlinear_range.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp, vp, i64, vp, vp]
         L.dptq_qlinear_range.restype = ctypes.c_int
         L.dptq_qlinear_fp6.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp]
         L.dptq_qlinear_fp6.restype = ctypes.c_int
@@ -566,10 +566,9 @@ def weight_sums(w_packed, out=None):
     return out
 
 
-def qlinear_range(codes, scales, zeros, bits, w_packed, w_scales, w_sums, y=None, acc=None):
-    """Quantized linear on range-quantized activations (zero-point corrected).
-    Returns y [M, N] fp16; for M > 16, acc (int32 [M, N] workspace) holds the
-    raw accumulator afterwards."""
+def qlinear_range(codes, scales, zeros, bits, w_packed, w_scales, w_sums, y=None):
+    """Quantized linear on range-quantized activations (zero-point corrected
+    in the GEMM epilogue).  Returns y [M, N] fp16."""
     torch = _torch()
     M = scales.shape[0]
     N, K2 = w_packed.shape
@@ -582,12 +581,8 @@ def qlinear_range(codes, scales, zeros, bits, w_packed, w_scales, w_sums, y=None
     _require(w_sums, "w_sums", torch.int32, (N,))
     if y is None:
         y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
-    if acc is None and M > 16:   # decode shapes need no workspace
-        acc = torch.empty((M, N), dtype=torch.int32, device=codes.device)
     _require(y, "y", torch.float16, (M, N))
-    if acc is not None:
-        _require(acc, "acc", torch.int32, (M, N))
     _check(lib().dptq_qlinear_range(_ptr(codes), _ptr(scales), _ptr(zeros), M, K, int(bits),
-                                    _ptr(w_packed), _ptr(w_scales), _ptr(w_sums), N, _ptr(acc),
-                                    _ptr(y), _stream(codes)), "dptq_qlinear_range")
+                                    _ptr(w_packed), _ptr(w_scales), _ptr(w_sums), N, _ptr(y),
+                                    _stream(codes)), "dptq_qlinear_range")
     return y

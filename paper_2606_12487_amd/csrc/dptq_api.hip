@@ -343,26 +343,17 @@ int dptq_weight_sums(const uint8_t* w_packed, int64_t N, int64_t K, int32_t* w_s
 
 int dptq_qlinear_range(const void* codes, const float* a_scales, const int32_t* a_zeros, int64_t M,
                        int64_t K, int32_t bits, const uint8_t* w_packed, const float* w_scales,
-                       const int32_t* w_sums, int64_t N, int32_t* acc, void* y, void* stream) {
+                       const int32_t* w_sums, int64_t N, void* y, void* stream) {
   int st = check_gemm_shape(M, K, bits, N);
   if (st != DPTQ_OK) return st;
   if (M == 0) return DPTQ_OK;
-  const bool decode = M <= 16;   // one launch, the correction in the decode GEMM's epilogue
-  if (!codes || !a_scales || !a_zeros || !w_packed || !w_scales || !w_sums || !y ||
-      (!decode && !acc))
+  if (!codes || !a_scales || !a_zeros || !w_packed || !w_scales || !w_sums || !y)
     return DPTQ_ERR_INVALID_ARG;
-  if (!aligned16(codes) || !aligned4(a_scales) || !aligned4(a_zeros) || !aligned16(w_packed) ||
-      !aligned16(w_scales) || !aligned16(w_sums) || (acc && !aligned16(acc)) || !aligned16(y))
+  if (!aligned16(codes) || !aligned16(a_scales) || !aligned4(a_zeros) || !aligned16(w_packed) ||
+      !aligned16(w_scales) || !aligned16(w_sums) || !aligned16(y))
     return DPTQ_ERR_INVALID_ARG;
-  const hipStream_t s = static_cast<hipStream_t>(stream);
-  if (decode)
-    return from_hip(dptq::launch_qlinear_zp_decode(codes, a_scales, a_zeros, M, (int)K, bits, w_packed,
-                                                   w_scales, w_sums, N, y, s));
-  hipError_t e = dptq::launch_qlinear(codes, nullptr, M, (int)K, bits, w_packed, nullptr, N, nullptr,
-                                      acc, dptq::kGemmAuto, s);
-  if (e != hipSuccess) return from_hip(e);
-  return from_hip(dptq::launch_range_epilogue(acc, a_scales, a_zeros, bits, w_sums, w_scales, M, N,
-                                               y, s));
+  return from_hip(dptq::launch_qlinear_zp(codes, a_scales, a_zeros, M, (int)K, bits, w_packed, w_scales,
+                                          w_sums, N, y, static_cast<hipStream_t>(stream)));
 }
 
 int dptq_layer_policy(int32_t num_layers, const uint8_t* mask, int32_t* bits_out) {

@@ -96,15 +96,12 @@ hipError_t launch_rotate_quant_range(const void* x, int64_t M, int K, HadSplit h
 // sums[n] = sum of weight row n's 4-bit codes (K % 32 == 0).
 hipError_t launch_weight_sums(const uint8_t* w_packed, int64_t N, int K, int32_t* sums,
                               hipStream_t stream);
-// Decode GEMM (M <= 16) with the zero-point correction in its epilogue.
-hipError_t launch_qlinear_zp_decode(const void* codes, const float* a_scales, const int32_t* a_zeros,
-                                   int64_t M, int K, int bits, const uint8_t* w_packed,
-                                   const float* w_scales, const int32_t* w_sums, int64_t N, void* y,
-                                   hipStream_t stream);
-// y = epilogue(acc + (2^(b-1) - zeros[m]) * w_sums[n]) from the raw accumulator.
-hipError_t launch_range_epilogue(const int32_t* acc, const float* a_scales, const int32_t* a_zeros,
-                                 int bits, const int32_t* w_sums, const float* w_scales, int64_t M,
-                                 int64_t N, void* y, hipStream_t stream);
+// The quantized linear with the zero-point correction in the GEMM epilogue
+// (any M; the kernel choice of launch_qlinear).
+hipError_t launch_qlinear_zp(const void* codes, const float* a_scales, const int32_t* a_zeros,
+                             int64_t M, int K, int bits, const uint8_t* w_packed,
+                             const float* w_scales, const int32_t* w_sums, int64_t N, void* y,
+                             hipStream_t stream);
 
 // Compute units of the current device (cached per device).
 int device_cus();

@@ -99,6 +99,27 @@ __device__ __forceinline__ __half dequant(int acc, float as, float ws) {
   return __float2half_rn(t2);
 }
 
+// Four accumulators of one lane (rows n .. n+3 of one column m), unscaled,
+// with the zero-point correction off * wz when ZP, dequantized and packed as
+// fp16.
+template <int BITS, bool ZP>
+__device__ __forceinline__ uint2 dequant4z(int a0, int a1, int a2, int a3, float as, float4 ws,
+                                           int off, int4 wz) {
+  int c0 = unscale<BITS>(a0), c1 = unscale<BITS>(a1), c2 = unscale<BITS>(a2), c3 = unscale<BITS>(a3);
+  if constexpr (ZP) {
+    c0 += off * wz.x;
+    c1 += off * wz.y;
+    c2 += off * wz.z;
+    c3 += off * wz.w;
+  }
+  const __half h0 = dequant(c0, as, ws.x), h1 = dequant(c1, as, ws.y);
+  const __half h2 = dequant(c2, as, ws.z), h3 = dequant(c3, as, ws.w);
+  uint2 pk;
+  pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
+  pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
+  return pk;
+}
+
 // ---------------------------------------------------------------------------
 // Prefill.  An output tile of BN (n) x BM (m) is computed by WN x WM
 // wavefronts, each owning a TI x TJ grid of 32 x 32 x 32 int8 MFMAs.  K is
@@ -202,11 +223,16 @@ struct Cfg {
 
 template <int BITS> using PrefillCfg = Cfg<BITS, 256, 128, 4, 2>;
 
-template <class C, bool ACC_OUT, bool WA8 = false>
+// ZP (the prefill kernels and the decode kernel alike): the range quantizer's
+// zero-point correction acc + (2^(BITS-1) - a_zeros[m]) * w_sums[n], exact in
+// int32, before the dequantization.
+template <class C, bool ACC_OUT, bool WA8 = false, bool ZP = false>
 __global__ void __launch_bounds__(C::kThreads)
 qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
               const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
-              int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
+              int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out,
+              const int32_t* __restrict__ a_zeros = nullptr,
+              const int32_t* __restrict__ w_sums = nullptr) {
   constexpr int BITS = C::kBits, kBN = C::kBN, kBM = C::kBM, kWN = C::kWN;
   constexpr int kTI = C::kTI, kTJ = C::kTJ, kWaves = C::kWaves, kThreads = C::kThreads;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[C::kLds];
@@ -461,20 +487,17 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
   for (int j = 0; j < kTJ; ++j) {
     const int ml = wm * kTJ * 32 + j * 32 + fr;
     const float as = a_scales[min(m0 + ml, M - 1)];
+    const int off = ZP ? (1 << (BITS - 1)) - a_zeros[min(m0 + ml, M - 1)] : 0;
 #pragma unroll
     for (int i = 0; i < kTI; ++i) {
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int nl = wn * kTI * 32 + i * 32 + 8 * b + 4 * fg;
         const float4 wsv = *reinterpret_cast<const float4*>(w_scales + min(n0 + nl, N - 4));
-        const __half h0 = dequant(unscale<BITS>(acc[i][j][4 * b]), as, wsv.x);
-        const __half h1 = dequant(unscale<BITS>(acc[i][j][4 * b + 1]), as, wsv.y);
-        const __half h2 = dequant(unscale<BITS>(acc[i][j][4 * b + 2]), as, wsv.z);
-        const __half h3 = dequant(unscale<BITS>(acc[i][j][4 * b + 3]), as, wsv.w);
-        uint2 pk;
-        pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
-        pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
-        *reinterpret_cast<uint2*>(smem + ml * C::kOutStride + nl * 2) = pk;
+        const int4 wz = ZP ? *reinterpret_cast<const int4*>(w_sums + min(n0 + nl, N - 4)) : make_int4(0, 0, 0, 0);
+        *reinterpret_cast<uint2*>(smem + ml * C::kOutStride + nl * 2) =
+            dequant4z<BITS, ZP>(acc[i][j][4 * b], acc[i][j][4 * b + 1], acc[i][j][4 * b + 2],
+                                acc[i][j][4 * b + 3], as, wsv, off, wz);
       }
     }
   }
@@ -561,24 +584,13 @@ __device__ __forceinline__ void sched_step() {
   }
 }
 
-// Four accumulators of one lane, dequantized and packed as fp16.
-template <int BITS>
-__device__ __forceinline__ uint2 dequant4(int a0, int a1, int a2, int a3, float as, float4 ws) {
-  const __half h0 = dequant(unscale<BITS>(a0), as, ws.x);
-  const __half h1 = dequant(unscale<BITS>(a1), as, ws.y);
-  const __half h2 = dequant(unscale<BITS>(a2), as, ws.z);
-  const __half h3 = dequant(unscale<BITS>(a3), as, ws.w);
-  uint2 pk;
-  pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
-  pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
-  return pk;
-}
-
-template <int BITS, bool ACC_OUT, bool WA8 = false>
+template <int BITS, bool ACC_OUT, bool WA8 = false, bool ZP = false>
 __global__ void __launch_bounds__(256)
 qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
                    const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
-                   int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out) {
+                   int M, int N, int K, __half* __restrict__ y, int32_t* __restrict__ acc_out,
+                   const int32_t* __restrict__ a_zeros = nullptr,
+                   const int32_t* __restrict__ w_sums = nullptr) {
   using C = Wide<BITS>;
   constexpr int kTI = C::kTI, kTJ = C::kTJ, kB = C::kBufs;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[C::kLds];
@@ -754,6 +766,7 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
     for (int j = 0; j < kTJ; ++j) {
       const float as = sc[mbase + j * 32];
       const int m = m0 + mbase + j * 32;
+      const int off = ZP ? (1 << (BITS - 1)) - a_zeros[m] : 0;
 #pragma unroll
       for (int i = 0; i < kTI; ++i) {
 #pragma unroll
@@ -761,10 +774,15 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
           const int nl = nbase + i * 32 + 16 * p + 4 * fg;
           const float4 ws0 = *reinterpret_cast<const float4*>(sc + 256 + nl);
           const float4 ws1 = *reinterpret_cast<const float4*>(sc + 256 + nl + 8);
-          const uint2 x0 = dequant4<BITS>(acc[i][j][8 * p], acc[i][j][8 * p + 1], acc[i][j][8 * p + 2],
-                                          acc[i][j][8 * p + 3], as, ws0);
-          const uint2 x1 = dequant4<BITS>(acc[i][j][8 * p + 4], acc[i][j][8 * p + 5], acc[i][j][8 * p + 6],
-                                          acc[i][j][8 * p + 7], as, ws1);
+          int4 wz0 = make_int4(0, 0, 0, 0), wz1 = make_int4(0, 0, 0, 0);
+          if constexpr (ZP) {
+            wz0 = *reinterpret_cast<const int4*>(w_sums + n0 + nl);
+            wz1 = *reinterpret_cast<const int4*>(w_sums + n0 + nl + 8);
+          }
+          const uint2 x0 = dequant4z<BITS, ZP>(acc[i][j][8 * p], acc[i][j][8 * p + 1], acc[i][j][8 * p + 2],
+                                               acc[i][j][8 * p + 3], as, ws0, off, wz0);
+          const uint2 x1 = dequant4z<BITS, ZP>(acc[i][j][8 * p + 4], acc[i][j][8 * p + 5],
+                                               acc[i][j][8 * p + 6], acc[i][j][8 * p + 7], as, ws1, off, wz1);
           const auto s0 = __builtin_amdgcn_permlane32_swap(x0.x, x1.x, false, false);
           const auto s1 = __builtin_amdgcn_permlane32_swap(x0.y, x1.y, false, false);
           const int n = n0 + nbase + i * 32 + 16 * p + 8 * fg;
@@ -991,19 +1009,20 @@ int decode_blocks(int64_t M, int64_t N, int bits, int cus) {
   return 1;
 }
 
-template <int BITS, bool ACC_OUT, bool WA8>
+template <int BITS, bool ACC_OUT, bool WA8, bool ZP>
 void launch_decode(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
-                   const float* ws, int64_t N, __half* y, int32_t* acc, hipStream_t stream) {
+                   const float* ws, int64_t N, __half* y, int32_t* acc, const int32_t* az,
+                   const int32_t* wsum, hipStream_t stream) {
   switch (decode_blocks(M, N, BITS, device_cus())) {
     case 2:
-      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, false, WA8, 2>), dim3((unsigned)(N / 32)),
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 2>), dim3((unsigned)(N / 32)),
                          dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
-                         nullptr, nullptr);
+                         az, wsum);
       break;
     default:
-      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, false, WA8, 1>), dim3((unsigned)(N / 16)),
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 1>), dim3((unsigned)(N / 16)),
                          dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
-                         nullptr, nullptr);
+                         az, wsum);
       break;
   }
 }
@@ -1026,22 +1045,24 @@ pack_w4_a8_kernel(const uint32_t* __restrict__ w, int64_t ndw, uint32_t* __restr
   out[i] = o;
 }
 
-template <class C, bool ACC_OUT, bool WA8 = false>
+template <class C, bool ACC_OUT, bool WA8, bool ZP>
 void launch_prefill(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
-                    const float* ws, int64_t N, __half* y, int32_t* acc, hipStream_t stream) {
+                    const float* ws, int64_t N, __half* y, int32_t* acc, const int32_t* az,
+                    const int32_t* wsum, hipStream_t stream) {
   const int64_t tiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
-  hipLaunchKernelGGL((qgemm_prefill<C, ACC_OUT, WA8>), dim3((unsigned)tiles), dim3(C::kThreads), 0,
-                     stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+  hipLaunchKernelGGL((qgemm_prefill<C, ACC_OUT, WA8, ZP>), dim3((unsigned)tiles), dim3(C::kThreads), 0,
+                     stream, a, as, w, ws, (int)M, (int)N, K, y, acc, az, wsum);
 }
 
-template <int BITS, bool ACC_OUT, bool WA8 = false>
+template <int BITS, bool ACC_OUT, bool WA8, bool ZP>
 void launch_wide(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
-                 const float* ws, int64_t N, __half* y, int32_t* acc, int cus, hipStream_t stream) {
+                 const float* ws, int64_t N, __half* y, int32_t* acc, const int32_t* az,
+                 const int32_t* wsum, int cus, hipStream_t stream) {
   using C = Wide<BITS>;
   const int64_t tiles = ((M + C::kBM - 1) / C::kBM) * ((N + C::kBN - 1) / C::kBN);
   const int64_t grid = tiles < cus ? tiles : cus;
-  hipLaunchKernelGGL((qgemm_prefill_wide<BITS, ACC_OUT, WA8>), dim3((unsigned)grid), dim3(C::kThreads), 0,
-                     stream, a, as, w, ws, (int)M, (int)N, K, y, acc);
+  hipLaunchKernelGGL((qgemm_prefill_wide<BITS, ACC_OUT, WA8, ZP>), dim3((unsigned)grid), dim3(C::kThreads),
+                     0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc, az, wsum);
 }
 
 // Relative time of a launch: rounds of one tile per compute unit, times the
@@ -1076,21 +1097,22 @@ int auto_kernel(int64_t M, int64_t N, int K) {
   return kGemmTile;
 }
 
-template <int BITS, bool ACC_OUT, bool WA8 = false>
+template <int BITS, bool ACC_OUT, bool WA8 = false, bool ZP = false>
 hipError_t launch_t(const uint8_t* a, const float* as, int64_t M, int K,
                     const uint8_t* w, const float* ws, int64_t N, __half* y,
-                    int32_t* acc, int kernel, hipStream_t stream) {
+                    int32_t* acc, int kernel, hipStream_t stream,
+                    const int32_t* az = nullptr, const int32_t* wsum = nullptr) {
   if (M == 0) return hipSuccess;
   if (kernel == kGemmAuto) kernel = auto_kernel<BITS>(M, N, K);
   switch (kernel) {
     case kGemmDecode:
-      launch_decode<BITS, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, stream);
+      launch_decode<BITS, ACC_OUT, WA8, ZP>(a, as, M, K, w, ws, N, y, acc, az, wsum, stream);
       break;
     case kGemmWide:
-      launch_wide<BITS, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, device_cus(), stream);
+      launch_wide<BITS, ACC_OUT, WA8, ZP>(a, as, M, K, w, ws, N, y, acc, az, wsum, device_cus(), stream);
       break;
     default:
-      launch_prefill<PrefillCfg<BITS>, ACC_OUT, WA8>(a, as, M, K, w, ws, N, y, acc, stream);
+      launch_prefill<PrefillCfg<BITS>, ACC_OUT, WA8, ZP>(a, as, M, K, w, ws, N, y, acc, az, wsum, stream);
       break;
   }
   return hipGetLastError();
@@ -1126,22 +1148,17 @@ bool gemm_kernel_fits(int kernel, int64_t M, int64_t N, int K, int bits) {
   }
 }
 
-hipError_t launch_qlinear_zp_decode(const void* codes, const float* a_scales, const int32_t* a_zeros,
-                                   int64_t M, int K, int bits, const uint8_t* w_packed,
-                                   const float* w_scales, const int32_t* w_sums, int64_t N, void* y,
-                                   hipStream_t stream) {
-  if (M == 0) return hipSuccess;
+hipError_t launch_qlinear_zp(const void* codes, const float* a_scales, const int32_t* a_zeros,
+                             int64_t M, int K, int bits, const uint8_t* w_packed,
+                             const float* w_scales, const int32_t* w_sums, int64_t N, void* y,
+                             hipStream_t stream) {
   const uint8_t* a = static_cast<const uint8_t*>(codes);
   __half* yh = static_cast<__half*>(y);
   if (bits == 4)
-    hipLaunchKernelGGL((qgemm_decode<4, false, true>), dim3((unsigned)(N / 16)), dim3(kDecWaves * 64), 0,
-                       stream, a, a_scales, w_packed, w_scales, (int)M, (int)N, K, yh, nullptr, a_zeros,
-                       w_sums);
-  else
-    hipLaunchKernelGGL((qgemm_decode<8, false, true>), dim3((unsigned)(N / 16)), dim3(kDecWaves * 64), 0,
-                       stream, a, a_scales, w_packed, w_scales, (int)M, (int)N, K, yh, nullptr, a_zeros,
-                       w_sums);
-  return hipGetLastError();
+    return launch_t<4, false, false, true>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr,
+                                           kGemmAuto, stream, a_zeros, w_sums);
+  return launch_t<8, false, false, true>(a, a_scales, M, K, w_packed, w_scales, N, yh, nullptr,
+                                         kGemmAuto, stream, a_zeros, w_sums);
 }
 
 hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M, int K,

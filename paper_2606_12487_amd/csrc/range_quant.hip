@@ -13,7 +13,9 @@
 // GEMM: sum_k (q_k - z) w_k = acc + (2^(b-1) - z) wsum[n], with acc the exact
 // accumulator of the stored codes and wsum[n] the sum of weight row n's
 // codes; the corrected sum is exact in int32, and the epilogue is the
-// symmetric path's, fl16(fl32(fl32(fl32(acc') * s_m) * w_s[n])).
+// symmetric path's, fl16(fl32(fl32(fl32(acc') * s_m) * w_s[n])).  The
+// correction runs in the GEMM kernels' epilogues (qgemm.hip); this file
+// holds the quantizer and the weight sums.
 
 #include "internal.h"
 #include "quant_device.h"
@@ -112,42 +114,6 @@ weight_sums_kernel(const uint8_t* __restrict__ w, int N, int K, int32_t* __restr
   if (lane == 0) out[n] = s;
 }
 
-// fl16(fl32(fl32(fl32(acc) * as) * ws)); the empty asm keeps the last product
-// an fp32 value (no fused multiply-convert to fp16).
-__device__ __forceinline__ __half range_dequant(int acc, float as, float ws) {
-  const float t1 = (float)acc * as;
-  float t2 = t1 * ws;
-  asm("" : "+v"(t2));
-  return __float2half_rn(t2);
-}
-
-// y[m, n] from acc[m, n] + (2^(b-1) - z[m]) wsum[n]; four consecutive n per
-// thread (N % 16 == 0).
-template <int BITS>
-__global__ void __launch_bounds__(256)
-range_epilogue_kernel(const int32_t* __restrict__ acc, const float* __restrict__ a_scales,
-                      const int32_t* __restrict__ a_zeros, const int32_t* __restrict__ w_sums,
-                      const float* __restrict__ w_scales, int64_t M, int N, __half* __restrict__ y) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // group of 4 outputs
-  const int64_t groups = M * (N / 4);
-  if (i >= groups) return;
-  const int64_t m = i / (N / 4);
-  const int n = (int)(i - m * (N / 4)) * 4;
-  const int off = (1 << (BITS - 1)) - a_zeros[m];
-  const float as = a_scales[m];
-  const int4 a = *reinterpret_cast<const int4*>(acc + m * N + n);
-  const int4 ws = *reinterpret_cast<const int4*>(w_sums + n);
-  const float4 sc = *reinterpret_cast<const float4*>(w_scales + n);
-  const __half h0 = range_dequant(a.x + off * ws.x, as, sc.x);
-  const __half h1 = range_dequant(a.y + off * ws.y, as, sc.y);
-  const __half h2 = range_dequant(a.z + off * ws.z, as, sc.z);
-  const __half h3 = range_dequant(a.w + off * ws.w, as, sc.w);
-  uint2 pk;
-  pk.x = (uint32_t)__half_as_ushort(h0) | ((uint32_t)__half_as_ushort(h1) << 16);
-  pk.y = (uint32_t)__half_as_ushort(h2) | ((uint32_t)__half_as_ushort(h3) << 16);
-  *reinterpret_cast<uint2*>(y + m * N + n) = pk;
-}
-
 size_t range_lds_bytes(int K) { return (size_t)((K + kSeg - 1) / kSeg) * kSegFloats * sizeof(float); }
 
 template <int BITS, int JP, bool F28>
@@ -200,22 +166,6 @@ hipError_t launch_weight_sums(const uint8_t* w_packed, int64_t N, int K, int32_t
   if (N == 0) return hipSuccess;
   hipLaunchKernelGGL(weight_sums_kernel, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, stream,
                      w_packed, (int)N, K, sums);
-  return hipGetLastError();
-}
-
-hipError_t launch_range_epilogue(const int32_t* acc, const float* a_scales, const int32_t* a_zeros,
-                                 int bits, const int32_t* w_sums, const float* w_scales, int64_t M,
-                                 int64_t N, void* y, hipStream_t stream) {
-  const int64_t groups = M * (N / 4);
-  if (groups == 0) return hipSuccess;
-  const unsigned grid = (unsigned)((groups + 255) / 256);
-  __half* out = static_cast<__half*>(y);
-  if (bits == 4)
-    hipLaunchKernelGGL(range_epilogue_kernel<4>, dim3(grid), dim3(256), 0, stream, acc, a_scales,
-                       a_zeros, w_sums, w_scales, M, (int)N, out);
-  else
-    hipLaunchKernelGGL(range_epilogue_kernel<8>, dim3(grid), dim3(256), 0, stream, acc, a_scales,
-                       a_zeros, w_sums, w_scales, M, (int)N, out);
   return hipGetLastError();
 }
 

@@ -316,12 +316,12 @@ def test_range_entry_points_validation(L):
     assert L.dptq_weight_sums(MISALIGNED, 4, 64, FAKE, NULL) == INVALID
     assert L.dptq_weight_sums(NULL, 0, 64, NULL, NULL) == OK
 
-    def ql(M=4, K=256, bits=4, N=32, acc=FAKE, y=FAKE, sums=FAKE):
-        return L.dptq_qlinear_range(FAKE, FAKE, FAKE, M, K, bits, FAKE, FAKE, sums, N, acc, y, NULL)
+    def ql(M=4, K=256, bits=4, N=32, y=FAKE, sums=FAKE, scales=FAKE):
+        return L.dptq_qlinear_range(FAKE, scales, FAKE, M, K, bits, FAKE, FAKE, sums, N, y, NULL)
     assert ql(K=200) == UNSUPPORTED
     assert ql(N=24) == UNSUPPORTED
     assert ql(bits=6) == INVALID
-    assert ql(M=17, acc=NULL) == INVALID    # prefill needs the accumulator workspace
     assert ql(sums=NULL) == INVALID
     assert ql(y=MISALIGNED) == INVALID
-    assert ql(M=0, acc=NULL, y=NULL) == OK
+    assert ql(scales=MISALIGNED) == INVALID
+    assert ql(M=0, y=NULL) == OK

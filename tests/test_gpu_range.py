@@ -96,11 +96,12 @@ def test_weight_sums_match_oracle(dev, N, K):
 
 
 LINEAR_CASES = [
-    # (M, K, N, h): one launch with the correction in the decode GEMM
-    # (M <= 16), either side of that boundary, prefill tiles with ragged M,
-    # the tiny workload
-    (1, 4096, 512, 4096), (16, 256, 512, 256), (17, 512, 128, 512), (70, 4096, 320, 4096),
-    (300, 1024, 256, 1024),
+    # (M, K, N, h): the correction in the epilogue of the decode GEMM (M <= 16,
+    # one and two channel blocks per workgroup), of the 256 x 128 tiles
+    # (ragged M) and of the 192 x 256 tiles (every output checked), either
+    # side of the decode boundary, the tiny workload
+    (1, 4096, 512, 4096), (16, 256, 512, 256), (16, 256, 16384, 256), (17, 512, 128, 512),
+    (70, 4096, 320, 4096), (300, 1024, 256, 1024), (2048, 512, 12288, 512),
     (5, 14336, 64, 28 * 512),
 ]
 
