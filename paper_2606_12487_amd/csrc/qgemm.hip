@@ -652,6 +652,28 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
       (dma16_at<(uint32_t)(C::kW + I * 4096)>(at, aofs[I], base), ...);
     }(std::make_integer_sequence<int, C::kALoads>{});
   };
+  // Loads [I0, I1) of one stage (weights first, then activations), so that a
+  // stage's loads can be spread between its MFMAs instead of leaving in one
+  // burst.
+  auto issue_part = [&](auto i0c, auto i1c, const uint8_t* wtile, const uint8_t* atile, int st, int buf)
+      __attribute__((always_inline)) {
+    constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value;
+    const uint32_t base = smem_base + buf * C::kStage + wave * 1024;
+    const uint8_t* wt = wtile + (size_t)st * C::kWRow;
+    const uint8_t* at = atile + (size_t)st * C::kARow;
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      (
+          [&] {
+            if constexpr (I >= I0 && I < I1) {
+              if constexpr (I < C::kWLoads)
+                dma16_at<(uint32_t)(I * 4096)>(wt, wofs[I], base);
+              else
+                dma16_at<(uint32_t)(C::kW + (I - C::kWLoads) * 4096)>(at, aofs[I - C::kWLoads], base);
+            }
+          }(),
+          ...);
+    }(std::make_integer_sequence<int, C::kLoads>{});
+  };
   auto wtile_of = [&](int n0) __attribute__((always_inline)) { return w_packed + (size_t)n0 * wrow; };
   auto atile_of = [&](int m0) __attribute__((always_inline)) { return a_codes + (size_t)m0 * arow; };
   // Scales of a tile into slot q (only when producing y; the accumulator
@@ -840,16 +862,29 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
       lds_barrier();
       // Stage s + kB of this tile, or of the next one (after the last tile:
       // this tile's last stage again).
+      // Its loads leave in three parts spread over the rest of this stage;
+      // all of them are issued before the next wait, so the counts hold.
       const int si = s + kB;
       const bool in_next = si >= nst;
-      issue(in_next ? wt1 : wt0, in_next ? at1 : at0, in_next ? (has_next ? si - nst : nst - 1) : si, cur);
+      const uint8_t* iw = in_next ? wt1 : wt0;
+      const uint8_t* ia = in_next ? at1 : at0;
+      const int ist = in_next ? (has_next ? si - nst : nst - 1) : si;
+      constexpr int kP1 = (C::kLoads + 2) / 3, kP2 = kP1 + (C::kLoads - kP1 + 1) / 2;
+      issue_part(std::integral_constant<int, 0>{}, std::integral_constant<int, kP1>{}, iw, ia, ist, cur);
       read_chunk(nxt, 0, p0);
       mfmas(u0);
       unpack(p1, 1, u1);
       sched_step<0, kNM, kVH, kNH, kNR>();
+      __builtin_amdgcn_sched_barrier(0);
+      issue_part(std::integral_constant<int, kP1>{}, std::integral_constant<int, kP2>{}, iw, ia, ist, cur);
+      __builtin_amdgcn_sched_barrier(0);
       mfmas(u1);
       unpack(p0, 0, u0);
       sched_step<0, kNM, kVH, kNH, 0>();
+      __builtin_amdgcn_sched_barrier(0);
+      issue_part(std::integral_constant<int, kP2>{}, std::integral_constant<int, C::kLoads>{}, iw, ia, ist,
+                 cur);
+      __builtin_amdgcn_sched_barrier(0);
       cur = nxt;
     }
     {
