@@ -254,8 +254,10 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
   // Loads of one stage: kb of the tile whose first blocks are at wt / at,
   // into ring buffer buf.  Load q < 18 is part q % 3 of weight block q / 3,
   // load q >= 18 part of activation block (q - 18) / 3; it lands at q KiB.
-  auto issue = [&](const uint8_t* wt, const uint8_t* at, int rbw, int rba, int kb, int buf)
-      __attribute__((always_inline)) {
+  // Loads P0 .. P1 - 1 of this wavefront's NL.
+  auto issue_part = [&](const uint8_t* wt, const uint8_t* at, int rbw, int rba, int kb, int buf, auto p0c,
+                        auto p1c) __attribute__((always_inline)) {
+    constexpr int P0 = decltype(p0c)::value, P1 = decltype(p1c)::value;
     const uint8_t* wst = wt + (size_t)kb * wstride;
     const uint8_t* ast = at + (size_t)kb * astride;
     const uint32_t base = smem_base + buf * C::kStage;
@@ -267,11 +269,11 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
         f6_dma16((q < C::kWLoads ? wst : ast) + rel * 1024, lane16, base + q * 1024);
       };
       [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
-        (one(std::integral_constant<int, Q0 + I>{}), ...);
-      }(std::make_integer_sequence<int, NL>{});
+        (one(std::integral_constant<int, Q0 + P0 + I>{}), ...);
+      }(std::make_integer_sequence<int, P1 - P0>{});
     } else {
 #pragma unroll
-      for (int i = 0; i < NL; ++i) {
+      for (int i = P0; i < P1; ++i) {
         const int q = Q0 + i;
         const bool isa = q >= C::kWLoads;
         const int qq = isa ? q - C::kWLoads : q;
@@ -282,6 +284,10 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
         f6_dma16(src, lane16, base + q * 1024);
       }
     }
+  };
+  auto issue = [&](const uint8_t* wt, const uint8_t* at, int rbw, int rba, int kb, int buf)
+      __attribute__((always_inline)) {
+    issue_part(wt, at, rbw, rba, kb, buf, std::integral_constant<int, 0>{}, std::integral_constant<int, NL>{});
   };
   // Scales of tile r into slot r & 1 (only when producing y): wavefront 0
   // loads a_s [256], wavefront 1 w_s [192], 4 bytes per lane, rows clamped.
@@ -344,16 +350,25 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
     f6_wait_vmcnt<NL>();
     f6_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue(wt, at, rbw, rba, kbi, buf);
+    // The stage's loads leave in three parts between the operand reads; the
+    // reads are spread over the MFMAs, so the loads are too, instead of
+    // leaving in one burst ahead of them.
+    constexpr int kL1 = (NL + 2) / 3, kL2 = kL1 + (NL - kL1 + 1) / 2;
+    issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, 0>{}, std::integral_constant<int, kL1>{});
     const uint8_t* s = smem + nbuf * C::kStage;
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-#pragma unroll
-      for (int i = 0; i < kTI; ++i)
-        read_frag(s + st * 1536 + kWOff + i * kF6Block, nxt.w[st][i]);
-#pragma unroll
-      for (int j = 0; j < kTJ; ++j)
-        read_frag(s + st * 1536 + kAOff + j * kF6Block, nxt.a[st][j]);
+    for (int f = 0; f < 2 * (kTI + kTJ); ++f) {
+      const int st = f / (kTI + kTJ), x = f % (kTI + kTJ);
+      if (x < kTI)
+        read_frag(s + st * 1536 + kWOff + x * kF6Block, nxt.w[st][x]);
+      else
+        read_frag(s + st * 1536 + kAOff + (x - kTI) * kF6Block, nxt.a[st][x - kTI]);
+      if (f == 3)
+        issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, kL1>{},
+                   std::integral_constant<int, kL2>{});
+      if (f == 8)
+        issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, kL2>{},
+                   std::integral_constant<int, NL>{});
     }
 #pragma unroll
     for (int st = 0; st < 2; ++st)
