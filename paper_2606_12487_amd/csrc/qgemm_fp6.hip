@@ -181,6 +181,15 @@ __device__ __forceinline__ void f6_sched_mixed() {
   }
 }
 
+// The part of a stage's loads issued after operand read f when a stage's
+// frags reads carry its loads in parts (part k after read k * frags / parts
+// - 1), or 0 when none follows read f.
+constexpr int f6_part_after(int f, int frags, int parts) {
+  for (int k = 1; k < parts; ++k)
+    if (f == k * frags / parts - 1) return k;
+  return 0;
+}
+
 // One MFMA step: fp6 x fp6, E8M0 scale 128 (= 2) on both operands.
 __device__ __forceinline__ v16f_t mfma_f6(const uint32_t* w, const uint32_t* a, v16f_t c) {
   const v8i_t wa = {(int)w[0], (int)w[1], (int)w[2], (int)w[3], (int)w[4], (int)w[5], 0, 0};
@@ -343,6 +352,7 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
   // be in flight), so after the barrier the stage three ahead is issued into
   // this stage's buffer and the next stage is read into nxt, all between
   // this stage's 24 MFMAs.  The scheduling fences keep that order.
+  constexpr int kParts = 5;   // parts a stage's loads are issued in
   auto stage = [&](const Frag& cur, Frag& nxt, int buf, const uint8_t* wt, const uint8_t* at,
                    int rbw, int rba, int kbi) __attribute__((always_inline)) {
     const int nbuf = buf == 2 ? 0 : buf + 1;
@@ -350,26 +360,29 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
     f6_wait_vmcnt<NL>();
     f6_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    // The stage's loads leave in three parts between the operand reads; the
+    // The stage's loads leave in kParts parts between the operand reads; the
     // reads are spread over the MFMAs, so the loads are too, instead of
-    // leaving in one burst ahead of them.
-    constexpr int kL1 = (NL + 2) / 3, kL2 = kL1 + (NL - kL1 + 1) / 2;
-    issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, 0>{}, std::integral_constant<int, kL1>{});
+    // leaving in one burst ahead of them.  Part k holds loads
+    // [k NL / kParts, (k + 1) NL / kParts) and follows read k * kFrags / kParts - 1.
+    constexpr int kFrags = 2 * (kTI + kTJ);
     const uint8_t* s = smem + nbuf * C::kStage;
-#pragma unroll
-    for (int f = 0; f < 2 * (kTI + kTJ); ++f) {
-      const int st = f / (kTI + kTJ), x = f % (kTI + kTJ);
-      if (x < kTI)
-        read_frag(s + st * 1536 + kWOff + x * kF6Block, nxt.w[st][x]);
-      else
-        read_frag(s + st * 1536 + kAOff + (x - kTI) * kF6Block, nxt.a[st][x - kTI]);
-      if (f == 3)
-        issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, kL1>{},
-                   std::integral_constant<int, kL2>{});
-      if (f == 8)
-        issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, kL2>{},
-                   std::integral_constant<int, NL>{});
-    }
+    issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, 0>{},
+               std::integral_constant<int, NL / kParts>{});
+    [&]<int... F>(std::integer_sequence<int, F...>) __attribute__((always_inline)) {
+      (
+          [&] {
+            constexpr int st = F / (kTI + kTJ), x = F % (kTI + kTJ);
+            if constexpr (x < kTI)
+              read_frag(s + st * 1536 + kWOff + x * kF6Block, nxt.w[st][x]);
+            else
+              read_frag(s + st * 1536 + kAOff + (x - kTI) * kF6Block, nxt.a[st][x - kTI]);
+            constexpr int k = f6_part_after(F, kFrags, kParts);
+            if constexpr (k > 0)
+              issue_part(wt, at, rbw, rba, kbi, buf, std::integral_constant<int, k * NL / kParts>{},
+                         std::integral_constant<int, (k + 1) * NL / kParts>{});
+          }(),
+          ...);
+    }(std::make_integer_sequence<int, kFrags>{});
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
