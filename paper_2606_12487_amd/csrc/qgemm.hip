@@ -740,6 +740,21 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
       }
     }
   };
+  // Read r of read_chunk's sequence (weight fragments, then activation
+  // reads), so that other work can be placed between the reads.
+  auto read_one = [&](auto rc, int buf, int e, Packed& p) __attribute__((always_inline)) {
+    constexpr int r = decltype(rc)::value;
+    const uint8_t* s = smem + buf * C::kStage;
+    if constexpr (r < kTI) {
+      const uint4 v = *reinterpret_cast<const uint4*>(s + wv[e] + r * 32 * C::kWRow);
+      p.w[r][0] = v.x; p.w[r][1] = v.y; p.w[r][2] = v.z; p.w[r][3] = v.w;
+    } else {
+      constexpr int j = (r - kTI) / C::kAReads, q = (r - kTI) % C::kAReads;
+      const uint32_t off = BITS == 4 ? av[e] : av[2 * e + q];
+      const uint4 v = *reinterpret_cast<const uint4*>(s + off + j * 32 * C::kARow);
+      p.a[j][4 * q] = v.x; p.a[j][4 * q + 1] = v.y; p.a[j][4 * q + 2] = v.z; p.a[j][4 * q + 3] = v.w;
+    }
+  };
   // MFMA operands of step kk (32 k) of a chunk.
   auto unpack = [&](const Packed& p, int kk, Ops& o) __attribute__((always_inline)) {
 #pragma unroll
@@ -862,28 +877,43 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
       lds_barrier();
       // Stage s + kB of this tile, or of the next one (after the last tile:
       // this tile's last stage again).
-      // Its loads leave in three parts spread over the rest of this stage;
-      // all of them are issued before the next wait, so the counts hold.
+      // Its loads leave in five parts spread over the rest of this stage:
+      // after the barrier, between the reads of the next chunk (which the
+      // scheduling groups spread over the MFMAs), and after each group of
+      // 12 MFMAs.  All of them are issued before the next wait, so the
+      // counts hold.
       const int si = s + kB;
       const bool in_next = si >= nst;
       const uint8_t* iw = in_next ? wt1 : wt0;
       const uint8_t* ia = in_next ? at1 : at0;
       const int ist = in_next ? (has_next ? si - nst : nst - 1) : si;
-      constexpr int kP1 = (C::kLoads + 2) / 3, kP2 = kP1 + (C::kLoads - kP1 + 1) / 2;
-      issue_part(std::integral_constant<int, 0>{}, std::integral_constant<int, kP1>{}, iw, ia, ist, cur);
-      read_chunk(nxt, 0, p0);
+      constexpr int L = C::kLoads;
+      issue_part(std::integral_constant<int, 0>{}, std::integral_constant<int, L / 5>{}, iw, ia, ist, cur);
+      [&]<int... R>(std::integer_sequence<int, R...>) __attribute__((always_inline)) {
+        (
+            [&] {
+              read_one(std::integral_constant<int, R>{}, nxt, 0, p0);
+              if constexpr (R == kNR / 3)
+                issue_part(std::integral_constant<int, L / 5>{}, std::integral_constant<int, 2 * L / 5>{}, iw,
+                           ia, ist, cur);
+              if constexpr (R == 2 * kNR / 3)
+                issue_part(std::integral_constant<int, 2 * L / 5>{}, std::integral_constant<int, 3 * L / 5>{},
+                           iw, ia, ist, cur);
+            }(),
+            ...);
+      }(std::make_integer_sequence<int, kNR>{});
       mfmas(u0);
       unpack(p1, 1, u1);
       sched_step<0, kNM, kVH, kNH, kNR>();
       __builtin_amdgcn_sched_barrier(0);
-      issue_part(std::integral_constant<int, kP1>{}, std::integral_constant<int, kP2>{}, iw, ia, ist, cur);
+      issue_part(std::integral_constant<int, 3 * L / 5>{}, std::integral_constant<int, 4 * L / 5>{}, iw, ia, ist,
+                 cur);
       __builtin_amdgcn_sched_barrier(0);
       mfmas(u1);
       unpack(p0, 0, u0);
       sched_step<0, kNM, kVH, kNH, 0>();
       __builtin_amdgcn_sched_barrier(0);
-      issue_part(std::integral_constant<int, kP2>{}, std::integral_constant<int, C::kLoads>{}, iw, ia, ist,
-                 cur);
+      issue_part(std::integral_constant<int, 4 * L / 5>{}, std::integral_constant<int, L>{}, iw, ia, ist, cur);
       __builtin_amdgcn_sched_barrier(0);
       cur = nxt;
     }
