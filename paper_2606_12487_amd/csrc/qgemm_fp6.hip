@@ -136,6 +136,16 @@ __device__ __forceinline__ void f6_dma16(const void* sbase, uint32_t voff, uint3
                : "v"(voff), "s"(sbase), "s"(lds_off)
                : "memory", "m0");
 }
+// The same with the LDS destination a wavefront-uniform base plus a
+// compile-time offset, formed in M0 by one scalar add; the global address is
+// sbase + voff.
+template <uint32_t OFF>
+__device__ __forceinline__ void f6_dma16_at(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_add_u32 m0, %2, %3\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds_base), "i"(OFF)
+               : "memory", "m0", "scc");
+}
 __device__ __forceinline__ void f6_dma4(const void* sbase, uint32_t voff, uint32_t lds_off) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
                :
@@ -275,7 +285,10 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
       auto one = [&](auto qc) __attribute__((always_inline)) {
         constexpr int q = decltype(qc)::value;
         constexpr int rel = q < C::kWLoads ? q : q - C::kWLoads;
-        f6_dma16((q < C::kWLoads ? wst : ast) + rel * 1024, lane16, base + q * 1024);
+        // The block offset travels in the per-lane offset (one vector
+        // instruction) and the LDS offset in M0's add, so a load costs one
+        // scalar instruction beside it.
+        f6_dma16_at<(uint32_t)(q * 1024)>(q < C::kWLoads ? wst : ast, lane16 + (uint32_t)(rel * 1024), base);
       };
       [&]<int... I>(std::integer_sequence<int, I...>) __attribute__((always_inline)) {
         (one(std::integral_constant<int, Q0 + P0 + I>{}), ...);
