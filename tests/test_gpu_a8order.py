@@ -68,6 +68,8 @@ CASES = [
     (256, 512, 192), (300, 640, 208), (511, 1024, 400), (1024, 4096, 2048),
     # decode workgroups of two blocks of 16 channels
     (8, 512, 32768), (12, 256, 16384),
+    # 192 x 256 tiles with shifted edge tiles in m and n, several per compute unit
+    (2100, 256, 12304),
 ]
 
 

@@ -102,6 +102,8 @@ LINEAR_CASES = [
     # side of the decode boundary, the tiny workload
     (1, 4096, 512, 4096), (16, 256, 512, 256), (16, 256, 16384, 256), (17, 512, 128, 512),
     (70, 4096, 320, 4096), (300, 1024, 256, 1024), (2048, 512, 12288, 512),
+    # 192 x 256 tiles with shifted edge tiles in m and n (every output checked)
+    (2100, 256, 12304, 256),
     (5, 14336, 64, 28 * 512),
 ]
 
