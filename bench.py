@@ -568,7 +568,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the quantized linear has no multi-GPU path in this build", file=sys.stderr)
+              "the library has no multi-GPU path (the sharding plan is documented, not built)", file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2606_12487_amd as dptq
