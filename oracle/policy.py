@@ -2,7 +2,7 @@
 
 Algorithm 1 step 2: b_x = 8 for a layer in the sensitive set S, else 4; weights
 and KV caches stay at 4 bits (step 1).  Eq. 21 instantiates S = {1, 2, 3, L}
-with layers indexed from 1; the efficiency study (Section 4.8) lists the same
+with layers indexed from 1; the efficiency study (Section 4.9) lists the same
 set 0-indexed as {0, 1, 2, L-1}.  This module works 0-indexed.
 
 An explicit mask (nonzero = 8-bit) overrides the default set, for sets chosen

@@ -53,6 +53,31 @@ def test_paley_quadratic_residues_mod13():
     assert np.array_equal(q_row, expect)
 
 
+def test_paley28_diagonal_blocks_by_hand():
+    # The conference matrix C has a zero diagonal, so the 2 x 2 diagonal blocks
+    # of C (x) [[1,1],[1,-1]] + I_14 (x) G are G itself, G = [[1,-1],[-1,-1]].
+    # Negating G (or dropping it) still gives a symmetric Hadamard matrix, so
+    # only this literal pins the sign of the identity term.
+    H = paley28()
+    G = np.array([[1, -1], [-1, -1]])
+    for p in range(14):
+        assert np.array_equal(H[2 * p:2 * p + 2, 2 * p:2 * p + 2], G), f"diagonal block {p}"
+
+
+def test_paley28_rows_written_out():
+    # Rows 2 and 3 (block row 1) worked by hand: C[1, :] = [1, chi(0), ...,
+    # chi(12)] = [1, 0, 1,-1, 1, 1,-1,-1,-1,-1, 1, 1,-1, 1] (squares mod 13 are
+    # 1, 3, 4, 9, 10, 12); block q contributes C[1,q]*[1, 1] and C[1,q]*[1,-1]
+    # off the diagonal and G's rows [1,-1], [-1,-1] on it (q = 1).  Row 0 is
+    # [1,-1] followed by thirteen [1, 1] blocks.
+    def parse(s):
+        return np.array([1 if ch == "+" else -1 for ch in s.replace(" ", "")])
+    H = paley28()
+    assert np.array_equal(H[0], parse("+- ++ ++ ++ ++ ++ ++ ++ ++ ++ ++ ++ ++ ++"))
+    assert np.array_equal(H[2], parse("++ +- ++ -- ++ ++ -- -- -- -- ++ ++ -- ++"))
+    assert np.array_equal(H[3], parse("+- -- +- -+ +- +- -+ -+ -+ -+ +- +- -+ +-"))
+
+
 @pytest.mark.parametrize("h", [28, 56, 112, 448, 896, 28 * 128])
 def test_kronecker_hadamard_orthogonal(h):
     # fp64 products of +-1 matrices are exact (sums of at most h < 2^53 terms).
