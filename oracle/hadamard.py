@@ -110,17 +110,8 @@ def hadamard(h):
     return np.kron(paley28(), Hp)
 
 
-def _tree_sum_axis0(P):
-    """Pairwise fp32 sum over axis 0 in index order: adjacent pairs first."""
-    assert P.dtype == np.float32
-    while P.shape[0] > 1:
-        assert P.shape[0] % 2 == 0
-        P = P[0::2] + P[1::2]
-    return P[0]
-
-
 @functools.lru_cache(maxsize=4)
-def _column_chunks(p, chunk_elems=1 << 22):
+def _column_chunks(p, chunk_elems=1 << 20):
     cols = max(1, chunk_elems // p)
     out = []
     for d0 in range(0, p, cols):
@@ -131,9 +122,12 @@ def _column_chunks(p, chunk_elems=1 << 22):
     return tuple(out) if p * p <= (1 << 26) else None
 
 
-def _rotate_block_fast_index(xa, p, chunk_elems=1 << 22):
-    """z[d] = sum_c xa[c] * H_p[c, d], pairwise tree over c (fp32)."""
-    z = np.empty(p, dtype=np.float32)
+def _rotate_fast_index(xa, p, chunk_elems=1 << 20, batch_elems=1 << 20):
+    """z[r, d] = sum_c xa[r, c] * H_p[c, d] for every row r, pairwise tree over c
+    in index order (fp32).  Rows are independent; they are only grouped so
+    that one array operation covers several of them."""
+    B = xa.shape[0]
+    z = np.empty((B, p), dtype=np.float32)
     chunks = _column_chunks(p)
     if chunks is None:   # large orders: regenerate columns instead of caching them
         cols = max(1, chunk_elems // p)
@@ -141,8 +135,12 @@ def _rotate_block_fast_index(xa, p, chunk_elems=1 << 22):
     for d0, d1, H in chunks:
         if H is None:
             H = sylvester_columns(p, d0, d1)
-        P = xa[:, None] * H                     # exact: entries are +-1
-        z[d0:d1] = _tree_sum_axis0(P)
+        rb = max(1, batch_elems // (p * (d1 - d0)))
+        for r0 in range(0, B, rb):
+            P = xa[r0:r0 + rb, :, None] * H[None]       # exact: entries are +-1
+            while P.shape[1] > 1:                       # adjacent pairs first
+                P = P[:, 0::2] + P[:, 1::2]
+            z[r0:r0 + rb, d0:d1] = P[:, 0]
     return z
 
 
@@ -150,6 +148,8 @@ def rotate_rows(x, h):
     """y = x . (I_{K/h} (x) H_h) for every row of x, in fp32 with the pinned order.
 
     x: [M, K] float16 or float32 (K a multiple of h).  Returns float32 [M, K].
+    Every length-h block of every row is rotated on its own; the blocks are
+    only stacked so that the same sums run as whole-array operations.
     """
     x = np.asarray(x)
     if x.ndim != 2:
@@ -158,21 +158,16 @@ def rotate_rows(x, h):
     f, p = split_had_size(h)
     if K % h != 0:
         raise ValueError(f"K={K} is not a multiple of the Hadamard size {h}")
-    x32 = x.astype(np.float32)                   # fp16 -> fp32 is exact
-    H28 = paley28().astype(np.float32) if f == 28 else None
-    y = np.empty((M, K), dtype=np.float32)
-    for m in range(M):
-        for blk in range(K // h):
-            xb = x32[m, blk * h:(blk + 1) * h].reshape(f, p)   # i = a*p + c
-            z = np.stack([_rotate_block_fast_index(xb[a], p) for a in range(f)])
-            if f == 1:
-                out = z[0]
-            else:
-                out = np.empty((f, p), dtype=np.float32)
-                for b in range(f):
-                    acc = H28[0, b] * z[0]
-                    for a in range(1, f):
-                        acc = acc + H28[a, b] * z[a]
-                    out[b] = acc
-            y[m, blk * h:(blk + 1) * h] = out.reshape(h)
-    return y
+    xb = x.astype(np.float32).reshape(M * (K // h), f, p)   # fp16 -> fp32 is exact; i = a*p + c
+    z = np.stack([_rotate_fast_index(np.ascontiguousarray(xb[:, a, :]), p) for a in range(f)],
+                 axis=1)                                     # [blocks, f, p]
+    if f == 1:
+        return z.reshape(M, K)
+    H28 = paley28().astype(np.float32)
+    out = np.empty_like(z)
+    for b in range(f):
+        acc = H28[0, b] * z[:, 0]
+        for a in range(1, f):                                # sequential over a = 0..27
+            acc = acc + H28[a, b] * z[:, a]
+        out[:, b] = acc
+    return out.reshape(M, K)
