@@ -482,6 +482,42 @@ int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int
                      const uint8_t* w_fp6, const float* w_scales, int64_t N, void* y,
                      int32_t* acc, void* stream);
 
+/* Device-native weight layouts of dptq_prepack_weights. */
+typedef enum {
+  DPTQ_WEIGHTS_FP6 = 1,     /* FP6 block layout: the 4-bit layers on dptq_qlinear_fp6 */
+  DPTQ_WEIGHTS_A8_ORDER = 2 /* 8-bit activation order: the 8-bit layers on dptq_qlinear_a8 */
+} dptq_weight_layout;
+
+/*
+ * dptq_prepacked_bytes - bytes of the dptq_prepack_weights output for an
+ * [N, K] weight matrix: dptq_fp6_bytes(N, K) for DPTQ_WEIGHTS_FP6 (rows padded
+ * to a multiple of 32), N * K / 2 for DPTQ_WEIGHTS_A8_ORDER.  -1 for an
+ * unknown layout, N < 0, or K not a multiple of 128 in [128, DPTQ_MAX_K].
+ */
+int64_t dptq_prepacked_bytes(int64_t N, int64_t K, int32_t layout);
+
+/*
+ * dptq_prepack_weights - the offline weights of Eq. 5 (rotated, quantized per
+ * output channel at 4 bits, Section 4.2; dptq_prepare_weights output) moved
+ * into the layout the GEMM of their layer reads natively.  The policy of
+ * Algorithm 1 step 2 / Eq. 21 fixes one activation width per layer, so each
+ * weight matrix needs one layout: DPTQ_WEIGHTS_FP6 for a 4-bit layer
+ * (dptq_qlinear_fp6), DPTQ_WEIGHTS_A8_ORDER for an 8-bit layer
+ * (dptq_qlinear_a8).  The codes are unchanged and so is every product: the
+ * call equals dptq_pack_fp6 or dptq_pack_w4_a8 on the same arguments.  Run
+ * once per weight matrix, offline.
+ *
+ *   w_packed device, uint8 [N, K/2] in the dptq_qlinear layout (low nibble =
+ *            even k), 16-byte aligned
+ *   N        rows >= 0 (0 enqueues nothing)
+ *   K        multiple of 128, 128 <= K <= DPTQ_MAX_K
+ *   layout   a dptq_weight_layout value, else DPTQ_ERR_INVALID_ARG
+ *   w_native device, dptq_prepacked_bytes(N, K, layout) bytes, 16-byte
+ *            aligned, must not overlap w_packed; the caller owns it
+ */
+int dptq_prepack_weights(const uint8_t* w_packed, int64_t N, int64_t K, int32_t layout,
+                         uint8_t* w_native, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,16 +30,23 @@ def _as_codes(codes, bits):
     raise ValueError(f"bits must be 4 or 8, got {bits}")
 
 
-def qlinear_acc_ref(a_codes, bits, w_packed):
-    """acc[m, n] = sum_k a[m, k] * w[n, k] exactly (int64 [M, N])."""
-    a = _as_codes(a_codes, bits)
-    w = unpack_int4(w_packed).astype(np.int64)
-    if a.shape[1] != w.shape[1]:
-        raise ValueError("K mismatch between activation codes and weights")
+def qlinear_acc_ref(a_codes, bits, w_packed, cols=8192):
+    """acc[m, n] = sum_k a[m, k] * w[n, k] exactly (int64 [M, N]).
+
+    The weight rows are taken `cols` output channels at a time; every entry is
+    one exact float64 dot product whatever the grouping."""
+    a = _as_codes(a_codes, bits).astype(np.float64)
     K = a.shape[1]
+    if 2 * np.asarray(w_packed).shape[1] != K:
+        raise ValueError("K mismatch between activation codes and weights")
     if K * 128 * 8 >= 2 ** 53:
         raise ValueError("K too large for an exact float64 accumulation")
-    return (a.astype(np.float64) @ w.astype(np.float64).T).astype(np.int64)
+    N = np.asarray(w_packed).shape[0]
+    out = np.empty((a.shape[0], N), dtype=np.int64)
+    for n0 in range(0, N, cols):
+        w = unpack_int4(w_packed[n0:n0 + cols]).astype(np.float64)
+        out[:, n0:n0 + cols] = (a @ w.T).astype(np.int64)
+    return out
 
 
 def qlinear_acc_entries(a_codes, bits, w_packed, rows, cols):

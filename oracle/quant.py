@@ -70,14 +70,12 @@ def pack_int4(codes):
 
 def unpack_int4(packed):
     """uint8 [..., K/2] -> int8 [..., K]: nibbles as 4-bit two's complement."""
-    p = np.asarray(packed, dtype=np.uint8).astype(np.int64)
-    lo = p & 0xF
-    hi = (p >> 4) & 0xF
-    lo = np.where(lo >= 8, lo - 16, lo)
-    hi = np.where(hi >= 8, hi - 16, hi)
+    p = np.asarray(packed, dtype=np.uint8)
+    nib = np.arange(16)
+    value = np.where(nib >= 8, nib - 16, nib).astype(np.int8)    # nibble -> -8..7
     out = np.empty(p.shape[:-1] + (2 * p.shape[-1],), dtype=np.int8)
-    out[..., 0::2] = lo
-    out[..., 1::2] = hi
+    out[..., 0::2] = value[p & 0xF]
+    out[..., 1::2] = value[p >> 4]
     return out
 
 

@@ -19,7 +19,8 @@ __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qline
            "kv_quant", "kv_dequant", "version", "fp6_bytes", "pack_fp6", "rotate_quant_fp6", "qlinear_fp6",
            "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "DECODE_AUTO", "DECODE_ONE_LAUNCH",
            "DECODE_TWO_LAUNCHES", "rotate_quant_range", "weight_sums", "qlinear_range",
-           "qlinear_fp6_acc", "pack_w4_a8", "qlinear_a8",
+           "qlinear_fp6_acc", "pack_w4_a8", "qlinear_a8", "prepacked_bytes", "prepack_weights",
+           "WEIGHTS_FP6", "WEIGHTS_A8_ORDER",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
@@ -37,10 +38,13 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed",
                       "dptq_qlinear_decode_fused", "dptq_rotate_quant_range",
                       "dptq_weight_sums", "dptq_qlinear_range", "dptq_pack_w4_a8",
-                      "dptq_qlinear_a8")
+                      "dptq_qlinear_a8", "dptq_prepacked_bytes", "dptq_prepack_weights")
 
 # Code layouts of dptq_rotate_quant_ex.
 LAYOUT_PACKED, LAYOUT_FP6 = 0, 1
+
+# Device-native weight layouts of dptq_prepack_weights.
+WEIGHTS_FP6, WEIGHTS_A8_ORDER = 1, 2
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
 GEMM_AUTO, GEMM_DECODE, GEMM_TILE_256X128, GEMM_TILE_192X256 = 0, 1, 2, 3
@@ -117,6 +121,10 @@ def lib():
         L.dptq_pack_w4_a8.restype = ctypes.c_int
         L.dptq_qlinear_a8.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, i32, vp]
         L.dptq_qlinear_a8.restype = ctypes.c_int
+        L.dptq_prepacked_bytes.argtypes = [i64, i64, i32]
+        L.dptq_prepacked_bytes.restype = ctypes.c_int64
+        L.dptq_prepack_weights.argtypes = [vp, i64, i64, i32, vp, vp]
+        L.dptq_prepack_weights.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -271,6 +279,32 @@ def pack_w4_a8(w_packed, out=None):
     _require(out, "out", torch.uint8, (N, K // 2))
     _check(lib().dptq_pack_w4_a8(_ptr(w_packed), N, K, _ptr(out), _stream(w_packed)),
            "dptq_pack_w4_a8")
+    return out
+
+
+def prepacked_bytes(N, K, layout):
+    """Bytes of the prepack_weights output for [N, K] weights in `layout`."""
+    n = lib().dptq_prepacked_bytes(int(N), int(K), int(layout))
+    if n < 0:
+        raise ValueError(f"no layout {layout} for N={N}, K={K} (K must be a multiple of 128)")
+    return n
+
+
+def prepack_weights(w_packed, layout, out=None):
+    """4-bit weights [N, K/2] in the qlinear layout -> the device-native layout
+    of their layer's GEMM (WEIGHTS_FP6 for qlinear_fp6, WEIGHTS_A8_ORDER for
+    qlinear_a8), uint8 [prepacked_bytes(N, K, layout)]."""
+    torch = _torch()
+    _require(w_packed, "w_packed", torch.uint8)
+    if w_packed.dim() != 2:
+        raise ValueError("w_packed must be 2-D [N, K/2]")
+    N, K = w_packed.shape[0], w_packed.shape[1] * 2
+    n = prepacked_bytes(N, K, layout)
+    if out is None:
+        out = torch.empty((n,), dtype=torch.uint8, device=w_packed.device)
+    _require(out, "out", torch.uint8, (n,))
+    _check(lib().dptq_prepack_weights(_ptr(w_packed), N, K, int(layout), _ptr(out),
+                                      _stream(w_packed)), "dptq_prepack_weights")
     return out
 
 

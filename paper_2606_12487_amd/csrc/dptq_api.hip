@@ -228,6 +228,20 @@ int dptq_pack_fp6(const uint8_t* codes, int64_t rows, int64_t K, uint8_t* out, v
   return from_hip(dptq::launch_pack_fp6(codes, rows, (int)K, out, static_cast<hipStream_t>(stream)));
 }
 
+int64_t dptq_prepacked_bytes(int64_t N, int64_t K, int32_t layout) {
+  if (N < 0 || K < 128 || K % 128 != 0 || K > DPTQ_MAX_K) return -1;
+  if (layout == DPTQ_WEIGHTS_FP6) return dptq_fp6_bytes(N, K);
+  if (layout == DPTQ_WEIGHTS_A8_ORDER) return N > 0x7FFFFFF0 ? -1 : N * (K / 2);
+  return -1;
+}
+
+int dptq_prepack_weights(const uint8_t* w_packed, int64_t N, int64_t K, int32_t layout,
+                         uint8_t* w_native, void* stream) {
+  if (layout == DPTQ_WEIGHTS_FP6) return dptq_pack_fp6(w_packed, N, K, w_native, stream);
+  if (layout == DPTQ_WEIGHTS_A8_ORDER) return dptq_pack_w4_a8(w_packed, N, K, w_native, stream);
+  return DPTQ_ERR_INVALID_ARG;
+}
+
 int dptq_rotate_quant_fp6(const void* x, int64_t M, int64_t K, int32_t had_size, uint8_t* out,
                           float* a_scales, void* stream) {
   HadSplit hs{};

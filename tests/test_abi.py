@@ -257,6 +257,21 @@ def test_fp6_entry_points_validation(L):
     assert L.dptq_rotate_quant_fp6(FAKE, 4, 192, 64, FAKE, FAKE, NULL) == UNSUPPORTED
 
 
+def test_prepack_weights_validation(L):
+    assert L.dptq_prepacked_bytes(33, 256, 1) == L.dptq_fp6_bytes(33, 256)
+    assert L.dptq_prepacked_bytes(33, 256, 2) == 33 * 128
+    assert L.dptq_prepacked_bytes(33, 256, 0) == -1            # no such layout
+    assert L.dptq_prepacked_bytes(33, 200, 2) == -1            # K % 128 != 0
+    assert L.dptq_prepacked_bytes(-1, 256, 1) == -1
+    for layout in (1, 2):
+        assert L.dptq_prepack_weights(FAKE, 4, 192, layout, FAKE, NULL) == UNSUPPORTED
+        assert L.dptq_prepack_weights(MISALIGNED, 4, 256, layout, FAKE, NULL) == INVALID
+        assert L.dptq_prepack_weights(FAKE, 4, 256, layout, NULL, NULL) == INVALID
+        assert L.dptq_prepack_weights(NULL, 0, 256, layout, NULL, NULL) == OK   # nothing to do
+    assert L.dptq_prepack_weights(FAKE, 4, 256, 0, FAKE, NULL) == INVALID
+    assert L.dptq_prepack_weights(FAKE, 4, 256, 3, FAKE, NULL) == INVALID
+
+
 def test_a8order_entry_points_validation(L):
     pk = L.dptq_pack_w4_a8
     assert pk(FAKE, -1, 256, FAKE, NULL) == INVALID

@@ -37,6 +37,7 @@ def _h(t):
 
 
 def _assert_f16(got, ref, what):
+    assert np.isfinite(ref.astype(np.float32)).all(), f"{what}: expected outputs overflow fp16"
     g, r = got.view(np.uint16), ref.view(np.uint16)
     assert np.array_equal(g, r), f"{what}: {(g != r).sum()} outputs differ"
 

@@ -19,6 +19,7 @@ import workloads
 from oracle import (rotate_quant_ref, prepare_weights_ref, qlinear_acc_ref, epilogue_ref,
                     unpack_int4)
 from oracle.gemm import qlinear_acc_entries
+from paritylib import e2m3_table as _e2m3_table, fp6_layout_ref
 
 torch = pytest.importorskip("torch")
 dptq = pytest.importorskip("paper_2606_12487_amd")
@@ -39,50 +40,6 @@ def _d(a, dev):
 def _h(t):
     torch.cuda.synchronize()
     return t.cpu().numpy()
-
-
-def _e2m3_value(bits6):
-    s = -1.0 if bits6 & 0x20 else 1.0
-    e, m = (bits6 >> 3) & 3, bits6 & 7
-    return s * (m / 8.0 if e == 0 else 2.0 ** (e - 1) * (1.0 + m / 8.0))
-
-
-def _e2m3_table():
-    """Encoding of c / 2 for c = -8..7, found by decoding all 64 patterns."""
-    table = {}
-    for c in range(-8, 8):
-        hits = [b for b in range(64) if _e2m3_value(b) == c / 2.0 and not (c == 0 and b & 0x20)]
-        assert len(hits) == 1, (c, hits)
-        table[c] = hits[0]
-    return table
-
-
-def fp6_layout_ref(packed, K):
-    """Reference FP6 block layout of packed 4-bit codes [R, K/2] -> uint8 bytes."""
-    codes = unpack_int4(packed).astype(np.int64)             # [R, K], -8..7
-    R = codes.shape[0]
-    Rp = (R + 31) // 32 * 32
-    full = np.zeros((Rp, K), dtype=np.int64)
-    full[:R] = codes
-    tab = _e2m3_table()
-    lut = np.array([tab[c] for c in range(-8, 8)], dtype=np.uint64)
-    enc = lut[full + 8]                                      # [Rp, K] six-bit fields
-    nkb = K // 128
-    # k = 128 kb + 64 g + 32 s + j ; lane l = 32 g + r
-    e = enc.reshape(Rp // 32, 32, nkb, 2, 2, 32)             # rb, r, kb, g, s, j
-    e = e.transpose(0, 2, 4, 3, 1, 5).reshape(Rp // 32, nkb, 2, 64, 32)   # rb, kb, s, l, j
-    words = np.zeros(e.shape[:-1] + (3,), dtype=np.uint64)
-    for j in range(32):
-        pos = 6 * j
-        w, off = pos // 64, pos % 64
-        words[..., w] |= e[..., j] << np.uint64(off)
-        if off > 58:
-            words[..., w + 1] |= e[..., j] >> np.uint64(64 - off)
-    # plane c of half s holds bytes 8c..8c+7 (word c) of every lane, lane-major
-    planes = words.transpose(0, 1, 2, 4, 3).copy()           # rb, kb, s, c, l
-    blocks = planes.view(np.uint8).reshape(Rp // 32, nkb, 2 * 3 * 64 * 8)   # rb, kb, 3072
-    # blocks are stored k-block major: (kb, rb)
-    return blocks.transpose(1, 0, 2).reshape(-1)
 
 
 def test_e2m3_table_closed_form():

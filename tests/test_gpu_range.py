@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 import workloads
+from paritylib import safe_w_scales
 from oracle import (rotate_quant_range_ref, weight_sums_ref, qlinear_range_ref,
                     qlinear_acc_entries, zero_point_acc_ref, epilogue_ref)
 
@@ -133,8 +134,9 @@ def test_qlinear_range_full_shape_sampled(dev, bits):
     rng = np.random.default_rng(40 + bits)
     x = workloads.gauss_outliers(rng, M, K)
     wp = workloads.random_weight_bytes(rng, N, K)
-    ws = workloads.random_scales(rng, N)
     c_ref, s_ref, z_ref = rotate_quant_range_ref(x, h, bits)
+    # |q - z| < 2^b, twice the symmetric bound on |code|: halve the output limit
+    ws = safe_w_scales(rng, N, K, s_ref, bits, limit=15000.0)
     wpd = _d(wp, dev)
     codes, scales, zeros = dptq.rotate_quant_range(_d(x, dev), h, bits)
     assert np.array_equal(_h(codes), c_ref)
@@ -148,4 +150,5 @@ def test_qlinear_range_full_shape_sampled(dev, bits):
     accz = acc + ((1 << (bits - 1)) - z_ref[rows].astype(np.int64)) * sums[cols]
     want = np.array([epilogue_ref(np.array([[a]]), s_ref[[m]], ws[[n]])[0, 0]
                      for a, m, n in zip(accz, rows, cols)])
+    assert np.isfinite(want.astype(np.float32)).all()
     assert np.array_equal(y[rows, cols].view(np.uint16), want.view(np.uint16))

@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import workloads
+from paritylib import safe_w_scales, oracle_y
 from oracle import (rotate_quant_signed_ref, prepare_weights_signed_ref, qlinear_acc_ref,
                     epilogue_ref)
 
@@ -59,7 +60,7 @@ def test_signed_rotate_quant(dev, M, K, h, bits):
 @pytest.mark.parametrize("M,K,h", [(5, 256, 256), (33, 4096, 4096), (2, 14336, 28 * 512),
                                    (70, 8192, 8192)])
 def test_signed_rotate_quant_fp6_layout(dev, M, K, h):
-    from test_gpu_fp6 import fp6_layout_ref
+    from paritylib import fp6_layout_ref
     rng = np.random.default_rng(K + h + M)
     x = workloads.gauss_outliers(rng, M, K)
     signs = workloads.random_sign_bits(rng, K)
@@ -130,9 +131,9 @@ def _fused_case(dev, M, K, N, h, bits, mode):
     rng = np.random.default_rng(M * 31 + K + N + bits)
     x = workloads.student_t(rng, M, K) if h % 28 == 0 else workloads.gauss_outliers(rng, M, K)
     wp = workloads.random_weight_bytes(rng, N, K)
-    ws = workloads.random_scales(rng, N)
     c_ref, s_ref = rotate_quant_ref(x, h, bits)
-    y_ref = epilogue_ref(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
+    ws = safe_w_scales(rng, N, K, s_ref, bits)
+    y_ref = oracle_y(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
     y, codes, scales = dptq.qlinear_decode_fused(_d(x, dev), h, bits, _d(wp, dev), _d(ws, dev),
                                                  mode=mode)
     assert np.array_equal(_h(scales).view(np.uint32), s_ref.view(np.uint32))
@@ -173,7 +174,9 @@ def test_fused_decode_consecutive_calls(dev):
     K, N, h = 4096, 2048, 4096
     rng = np.random.default_rng(77)
     wp = workloads.random_weight_bytes(rng, N, K)
-    ws = workloads.random_scales(rng, N)
+    # a rotated entry is at most the L1 norm of its row's block (about 3.3e3
+    # for these rows), so 2e4 bounds the absmax of all four steps at once
+    ws = safe_w_scales(rng, N, K, np.array([20000.0 / 7.0], np.float32), 4)
     wpd, wsd = _d(wp, dev), _d(ws, dev)
     for step, M in enumerate([4, 1, 16, 7]):
         x = workloads.gauss_outliers(rng, M, K)
@@ -181,6 +184,6 @@ def test_fused_decode_consecutive_calls(dev):
         y, _, scales = dptq.qlinear_decode_fused(_d(x, dev), h, bits, wpd, wsd,
                                                  mode=dptq.DECODE_ONE_LAUNCH)
         c_ref, s_ref = rotate_quant_ref(x, h, bits)
-        y_ref = epilogue_ref(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
+        y_ref = oracle_y(qlinear_acc_ref(c_ref, bits, wp), s_ref, ws)
         assert np.array_equal(_h(y).view(np.uint16), y_ref.view(np.uint16)), f"step {step}"
         assert np.array_equal(_h(scales).view(np.uint32), s_ref.view(np.uint32))
