@@ -41,13 +41,13 @@ typedef __attribute__((address_space(3))) uint8_t* lds_ptr_t;
 constexpr int kF6Block = 3072;   // bytes of one 32-row x 128-k block
 
 // e2m3 encoding of c / 2 for the 4-bit two's complement nibble n (c = n for
-// n < 8, n - 16 otherwise), one byte per nibble value.
-constexpr uint64_t kE2m3Pos = 0x161412100C080400ull;   // c = 0 .. 7
-constexpr uint64_t kE2m3Neg = 0x24282C3032343638ull;   // c = -8 .. -1
-
+// n < 8, n - 16 otherwise): byte n & 3 of one of four dwords (c = 0..3, 4..7,
+// -8..-5, -4..-1).  Only 32-bit operations: the data path of this file uses
+// no 64-bit shifts.
 __device__ __forceinline__ uint32_t e2m3_half(uint32_t n) {
-  const uint64_t t = (n & 8u) ? kE2m3Neg : kE2m3Pos;
-  return (uint32_t)(t >> ((n & 7u) * 8u)) & 0x3Fu;
+  const uint32_t lo = (n & 8u) ? 0x32343638u : 0x0C080400u;
+  const uint32_t hi = (n & 8u) ? 0x24282C30u : 0x16141210u;
+  return (((n & 4u) ? hi : lo) >> ((n & 3u) * 8u)) & 0x3Fu;
 }
 
 // ---------------------------------------------------------------------------
@@ -76,22 +76,15 @@ pack_fp6_kernel(const uint8_t* __restrict__ codes, int R, int K, uint8_t* __rest
   uint8_t* base = out + blk * kF6Block;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
-    // Codes 32 h .. 32 h + 31 of the lane's 64: input dwords 4 h .. 4 h + 3.
-    uint32_t o[6];
-    uint64_t bits = 0;
-    int nb = 0, no = 0;
+    // Codes 32 h .. 32 h + 31 of the lane's 64 (input dwords 4 h .. 4 h + 3):
+    // field j occupies bits 6 j .. 6 j + 5 of the six output dwords.
+    uint32_t o[6] = {0u, 0u, 0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        bits |= (uint64_t)e2m3_half((w[4 * h + d] >> (4 * q)) & 15u) << nb;
-        nb += 6;
-        if (nb >= 32) {
-          o[no++] = (uint32_t)bits;
-          bits >>= 32;
-          nb -= 32;
-        }
-      }
+    for (int j = 0; j < 32; ++j) {
+      const uint32_t f = e2m3_half((w[4 * h + j / 8] >> (4 * (j % 8))) & 15u);
+      const int d = (6 * j) / 32, off = (6 * j) % 32;
+      o[d] |= f << off;
+      if (off > 26) o[d + 1] |= f >> (32 - off);
     }
 #pragma unroll
     for (int c = 0; c < 3; ++c)

@@ -161,3 +161,17 @@ def oracle_prepare(w, h):
     with ThreadPoolExecutor(WORKERS) as ex:
         parts = list(ex.map(lambda r: prepare_weights_ref(w[r[0]:r[-1] + 1], h), chunks))
     return np.concatenate([p[0] for p in parts]), np.concatenate([p[1] for p in parts])
+
+
+def assert_acc(got, ref, what):
+    """int32 accumulators against the oracle's, naming where they differ."""
+    g = np.asarray(got).astype(np.int64)
+    if np.array_equal(g, ref):
+        return
+    bad = np.nonzero(g != ref)
+    rows, cols = bad
+    raise AssertionError(
+        f"{what}: {rows.size} accumulators differ; rows {np.unique(rows)[:12]} "
+        f"({np.unique(rows).size} rows, 256-row tiles {np.unique(rows // 256)[:12]}), "
+        f"cols {np.unique(cols)[:12]} ({np.unique(cols).size} cols, 192-col tiles "
+        f"{np.unique(cols // 192)[:12]}); got {g[bad][:6]} want {ref[bad][:6]}")

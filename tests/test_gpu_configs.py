@@ -28,7 +28,7 @@ import numpy as np
 import pytest
 
 import workloads
-from paritylib import (sample_rows, oracle_rotate, oracle_codes, oracle_acc, oracle_y,
+from paritylib import (assert_acc, sample_rows, oracle_rotate, oracle_codes, oracle_acc, oracle_y,
                        oracle_prepare, safe_w_scales, assert_bytes, assert_f16,
                        fp6_layout_decode)
 from oracle import unpack_int4
@@ -109,12 +109,11 @@ def test_single_linear_every_row(dev, name, M):
         y_ref = oracle_y(acc_ref, s_ref, ws)
         for path, y in _gemm_paths(dev, bits, codes, scales, a6, wq, ws, M, K, N).items():
             assert_f16(y, y_ref, f"{what} y ({path})")
-        acc = _h(dptq.qlinear_acc(codes, bits, _d(wq, dev)))
-        assert np.array_equal(acc.astype(np.int64), acc_ref), f"{what}: accumulators differ"
+        wqd = _d(wq, dev)
+        assert_acc(_h(dptq.qlinear_acc(codes, bits, wqd)), acc_ref, what + " int8")
         if a6 is not None:
-            w6 = dptq.prepack_weights(_d(wq, dev), dptq.WEIGHTS_FP6)
-            acc6 = _h(dptq.qlinear_fp6_acc(a6, w6, M, K, N))
-            assert np.array_equal(acc6.astype(np.int64), acc_ref), f"{what}: FP6 accumulators differ"
+            w6 = dptq.prepack_weights(wqd, dptq.WEIGHTS_FP6)
+            assert_acc(_h(dptq.qlinear_fp6_acc(a6, w6, M, K, N)), acc_ref, what + " FP6")
 
 
 # ---------------------------------------------------------------------------
@@ -235,15 +234,11 @@ def test_full_accumulators(dev, name, M, K, N, bits):
     wq = workloads.random_weight_bytes(rng, N, K)
     acc_ref = oracle_acc(a, bits, wq)
     ad, wqd = _d(a, dev), _d(wq, dev)
-    acc = _h(dptq.qlinear_acc(ad, bits, wqd))
-    assert np.array_equal(acc.astype(np.int64), acc_ref), \
-        f"{name} A{bits}: {(acc != acc_ref).sum()} accumulators differ"
-    del acc
+    assert_acc(_h(dptq.qlinear_acc(ad, bits, wqd)), acc_ref, f"{name} A{bits} int8")
     if bits == 4:
         w6 = dptq.prepack_weights(wqd, dptq.WEIGHTS_FP6)
-        acc6 = _h(dptq.qlinear_fp6_acc(dptq.pack_fp6(ad), w6, M, K, N))
-        assert np.array_equal(acc6.astype(np.int64), acc_ref), \
-            f"{name} A4 FP6: {(acc6 != acc_ref).sum()} accumulators differ"
+        assert_acc(_h(dptq.qlinear_fp6_acc(dptq.pack_fp6(ad), w6, M, K, N)), acc_ref,
+                   f"{name} A4 FP6")
     else:
         a_s = workloads.random_scales(rng, M, 1e-3, 1.0)
         ws = safe_w_scales(rng, N, K, a_s, bits)
