@@ -1,37 +1,49 @@
 """Benchmark of the DynamicPTQ quantized linear layer on one MI355X.
 
-Workload (one "step"): the LLaMA-2-7B fused QKV projection, M = 2048 prefill
-tokens, K = 4096, N = 12288, Hadamard 4096, with synthetic seeded fp16
-activations (N(0,1) plus 4 outlier channels x50-x200) and N(0, 0.02) weights
-quantized to 4 bits per output channel.  The layer policy (Eq. 21) is looked
-up for a 32-layer model, and the step runs the layer as a non-sensitive layer
-(A4) and then as a sensitive layer (A8): per precision one rotate+quantize
-launch and one GEMM launch, all on one stream.  The A4 layer runs on the FP6
-matrix cores (rotate+quantize writing the FP6 operand layout, then the FP6
-GEMM against the same weights pre-packed once); the A8 layer on the int8
-matrix cores.  Both return the oracle's results bit for bit.  Inputs are resident in HBM
-before timing; the step cycles through enough copies of activations and
-weights (> 256 MiB) that the Infinity Cache cannot hold them.  The timed
-steps launch every kernel from the host on one stream; the same steps
-replayed from captured HIP graphs are reported under "graph".
+Headline workload (one "step"): every linear of the LLaMA-2-70B stack, 80
+layers x (fused QKV 8192 -> 10240, o 8192 -> 8192, gate/up 8192 -> 57344,
+down 28672 -> 8192 with the 28 x 1024 Hadamard), at M = 4096 prefill tokens.
+The per-layer activation precision comes from the policy (Eq. 21, Algorithm 1
+step 2) under a seeded mixed mask (4 of 80 layers at 8 bits).  Each linear
+runs rotate+quantize then the GEMM with its dequant epilogue: a 4-bit layer
+on the FP6 matrix cores (codes written straight into the FP6 operand layout,
+weights pre-packed into it once), an 8-bit layer on the int8 matrix cores
+(weights pre-packed into the 8-bit activation order once).  Both return the
+oracle's results bit for bit.  Weights are N(0, 0.02) fp32 drawn on the device
+(seeded), quantized to 4 bits per output channel by the library and resident
+in HBM (34 GB of packed codes, 85 GB with the device-native layouts); each
+linear's activations are the seeded fp16 input of that linear in the stack
+(N(0,1) with outlier channels; Student-t(3) for the down projection).
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--extended]
 
-Prints one JSON line.  value = total integer ops (2 M N K per GEMM) / time.
+Prints one JSON line.  value = total integer ops (2 M N K per linear) of a
+step / wall time per step, in TOPS.  The other workloads (the tiny layer, the
+LLaMA-2-7B QKV layer, the LLaMA-3-8B down projection at decode and prefill
+sizes, the LLaMA-2-7B 32-layer stack, the 70B stack at M = 8 decode) are
+reported under "configs", timed by graph-replayed launches.
 """
 
 import argparse
 import json
 import os
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, T ops/s
+PEAK_FP6_TOPS = 10100.0      # MI355X dense fp6 / fp4 MFMA, T ops/s
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, GB/s
+# fp32 vector issue without packed instructions (the kernels are built without
+# them): 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane-operations per second.
+PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9
 METRIC = "W4A4/W4A8 qlinear TOPS (rotate+quant+GEMM), % int8 MFMA peak; decode GB/s"
+HEADLINE = "llama2_70b_layer"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_fp6_llama2_70b_stack.txt")
+TRAFFIC_SOURCE = os.path.join(ROOT, "paper_2606_12487_amd", "csrc", "qgemm_fp6.hip")
 
 
 def parse():
@@ -39,23 +51,25 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--copies", type=int, default=12,
-                   help="distinct activation/weight copies cycled per step")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=160,
-                   help="token rows of the workload the CPU oracle is timed on")
+    p.add_argument("--cpu-workers", type=int, default=0,
+                   help="worker processes of the CPU oracle baseline (0: affinity count, at most 16)")
+    p.add_argument("--no-configs", action="store_true",
+                   help="time only the headline stack (no other workloads)")
     p.add_argument("--extended", action="store_true",
-                   help="also time the decode shapes, the fused decode, the range quantizer, "
-                        "calibration, KV4 and whole stacks")
-    p.add_argument("--only", choices=["rq4", "gemm4", "rq6", "gemm6", "rq8", "gemm8", "copy"],
-                   help="run one kernel of the step --steps times (for counter runs) "
-                        "or, with copy, a plain device copy of 256 MiB (counter calibration)")
+                   help="also time the fused decode paths, the range quantizer, calibration and KV4")
+    p.add_argument("--only", choices=["rq6", "gemm6", "rq8", "gemm8", "copy"],
+                   help="launch one kernel family of the headline step --steps times at every "
+                        "linear shape, nothing timed (for counter runs); copy: a 256 MiB device copy")
     return p.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_prefill_a8_llama2_7b_qkv.txt")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_12487_amd", "csrc", "qgemm.hip")
-PEAK_FP6_TOPS = 10100.0      # MI355X dense fp6 / fp4 MFMA, T ops/s
+# ---------------------------------------------------------------------------
+# helpers
+# ---------------------------------------------------------------------------
+def progress(msg):
+    """One line on stderr per finished phase (the JSON line alone goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def source_digest(path):
@@ -64,8 +78,8 @@ def source_digest(path):
 
 
 def measured_traffic():
-    """HBM bytes per launch of the A8 int8 GEMM from the committed counter summary,
-    or None when it is missing or was taken on a different kernel source."""
+    """Mean HBM bytes per launch of the headline's FP6 GEMM from the committed
+    counter summary, or None when it is missing or was taken on other sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     kv = {}
@@ -73,7 +87,7 @@ def measured_traffic():
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("source_sha256_16") != source_digest(KERNEL_SOURCE):
+    if kv.get("source_sha256_16") != source_digest(TRAFFIC_SOURCE):
         return None
     try:
         return int(float(kv["hbm_bytes_per_launch"]))
@@ -81,189 +95,52 @@ def measured_traffic():
         return None
 
 
-def run_only(torch, dptq, cfg, args):
-    """One kernel, repeated; nothing timed.  Used under rocprofv3 --pmc."""
-    import numpy as np
-    import workloads
-    dev = torch.device("cuda:0")
-    if args.only == "copy":
-        n = 256 << 20
-        src = torch.ones(n, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(args.steps):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"only": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n}))
-        return
-    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
-    rng = np.random.default_rng(cfg["seed"])
-    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
-    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
-    wp, ws = dptq.prepare_weights(w, h)
-    del w
-    y = torch.empty((M, N), dtype=torch.float16, device=dev)
-    if args.only.endswith("6"):
-        a6, s6 = dptq.rotate_quant_fp6(x, h)
-        w6 = dptq.pack_fp6(wp)
-        torch.cuda.synchronize()
-        for _ in range(args.steps):
-            if args.only.startswith("rq"):
-                dptq.rotate_quant_fp6(x, h, a6, s6)
-            else:
-                dptq.qlinear_fp6(a6, s6, w6, ws, M, K, N, y)
-        torch.cuda.synchronize()
-        print(json.dumps({"only": args.only, "launches": args.steps}))
-        return
-    bits = 4 if args.only.endswith("4") else 8
-    codes, scales = dptq.rotate_quant(x, h, bits)
-    w8 = dptq.pack_w4_a8(wp) if bits == 8 else None
-    torch.cuda.synchronize()
-    for _ in range(args.steps):
-        if args.only.startswith("rq"):
-            dptq.rotate_quant(x, h, bits, codes, scales)
-        elif bits == 8:
-            dptq.qlinear_a8(codes, scales, w8, ws, y)     # the step's A8 GEMM
-        else:
-            dptq.qlinear(codes, scales, bits, wp, ws, y)
-    torch.cuda.synchronize()
-    print(json.dumps({"only": args.only, "launches": args.steps}))
+class ClockSampler:
+    """sclk / mclk read from the GPU's metrics table every ~20 ms on a thread
+    while the timed steps run (MHz)."""
+
+    def __init__(self):
+        self.samples, self.error = [], None
+        self._stop = threading.Event()
+        self._t = None
+
+    def __enter__(self):
+        self._t = threading.Thread(target=self._run, daemon=True)
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join(timeout=5)
+
+    def _run(self):
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            try:
+                h = amdsmi.amdsmi_get_processor_handles()[0]
+                while not self._stop.is_set():
+                    m = amdsmi.amdsmi_get_gpu_metrics_info(h)
+                    self.samples.append((m.get("current_gfxclk"), m.get("average_gfxclk_frequency"),
+                                         m.get("current_uclk")))
+                    time.sleep(0.02)
+            finally:
+                amdsmi.amdsmi_shut_down()
+        except Exception as e:  # no metrics on this machine: reported, not fatal
+            self.error = repr(e)[:200]
+
+    def summary(self):
+        def col(i):
+            v = [s[i] for s in self.samples if isinstance(s[i], (int, float))]
+            return {"mean": round(sum(v) / len(v), 1), "min": min(v), "max": max(v)} if v else None
+        return {"samples": len(self.samples), "sclk_current_mhz": col(0),
+                "sclk_average_mhz": col(1), "mclk_mhz": col(2), "error": self.error}
 
 
-def _events(torch, n):
-    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-
-
-def time_layer(torch, dptq, cfg, args):
-    import numpy as np
-    import workloads
-    dev = torch.device("cuda:0")
-    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
-    rng = np.random.default_rng(cfg["seed"])
-    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
-    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
-    wp, ws = dptq.prepare_weights(w, h)
-    del w
-    R = max(1, args.copies)
-    xs = [x.clone() for _ in range(R)]
-    wps = [wp.clone() for _ in range(R)]
-    w6s = [dptq.pack_fp6(wp) for _ in range(R)]      # the same weights, FP6 operand layout
-    w8s = [dptq.pack_w4_a8(wp) for _ in range(R)]    # the same weights, 8-bit activation order
-    wss = [ws.clone() for _ in range(R)]
-    codes8 = torch.empty((M, K), dtype=torch.int8, device=dev)
-    a6 = torch.empty((dptq.fp6_bytes(M, K),), dtype=torch.uint8, device=dev)
-    scales = torch.empty((M,), dtype=torch.float32, device=dev)
-    y = torch.empty((M, N), dtype=torch.float16, device=dev)
-    torch.cuda.synchronize()
-
-    n_layers = 32
-    def layers(r, seq):
-        for bits in seq:
-            if bits == 4:
-                dptq.rotate_quant_fp6(xs[r], h, a6, scales)
-                dptq.qlinear_fp6(a6, scales, w6s[r], wss[r], M, K, N, y)
-            else:
-                dptq.rotate_quant(xs[r], h, bits, codes8, scales)
-                dptq.qlinear_a8(codes8, scales, w8s[r], wss[r], y)
-
-    def policy():
-        bits_all = dptq.layer_policy(n_layers)
-        return (bits_all[n_layers // 2], bits_all[0])     # a non-sensitive, a sensitive layer
-
-    # The timed steps: every kernel launched from the host on one stream.
-    seq = policy()
-    for i in range(args.warmup):
-        layers(i % R, policy())
-    torch.cuda.synchronize()
-    e0, e1 = _events(torch, 2)
-    t0 = time.perf_counter()
-    e0.record()
-    for i in range(args.steps):
-        layers(i % R, policy())
-    e1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms = e0.elapsed_time(e1)
-
-    # The same steps replayed from captured HIP graphs (one per input copy;
-    # the policy lookup stays on the host), for reference.  A replay must
-    # reproduce the eager result bit for bit.
-    s_cap = torch.cuda.Stream()
-    graphs = []
-    for r in range(R):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=s_cap):
-            layers(r, seq)
-        graphs.append(g)
-    layers(0, seq)
-    torch.cuda.synchronize()
-    y_eager = y.clone()
-    y.zero_()
-    graphs[0].replay()
-    torch.cuda.synchronize()
-    if not torch.equal(y.view(torch.int16), y_eager.view(torch.int16)):
-        raise RuntimeError("graph replay of the step differs from its eager launches")
-    for i in range(args.warmup):
-        graphs[i % R].replay()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        policy()
-        graphs[i % R].replay()
-    torch.cuda.synchronize()
-    wall_graph = time.perf_counter() - t0
-    del graphs
-    return wall, gpu_ms, seq, wall_graph
-
-
-def time_kernels(torch, dptq, cfg, args, seq, reps=24):
-    """Average duration (ms) of each kernel of the step, from `reps`
-    back-to-back launches captured in a HIP graph and replayed between two HIP
-    events on the launch stream (no host launch gaps, no events between the
-    launches).  Inputs cycle over the same copies as the step."""
-    import numpy as np
-    import workloads
-    dev = torch.device("cuda:0")
-    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
-    rng = np.random.default_rng(cfg["seed"] + 7)
-    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
-    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
-    wp, ws = dptq.prepare_weights(w, h)
-    del w
-    R = max(1, args.copies)
-    xs = [x.clone() for _ in range(R)]
-    wps = [wp.clone() for _ in range(R)]
-    w6s = [dptq.pack_fp6(wp) for _ in range(R)]
-    w8s = [dptq.pack_w4_a8(wp) for _ in range(R)]
-    y = torch.empty((M, N), dtype=torch.float16, device=dev)
-    out = {}
-    # the step's kernels: FP6 A4 layer, int8 A8 layer
-    a6, s6 = dptq.rotate_quant_fp6(x, h)
-    out["rotate_quant_fp6_a4"] = _graph_time(torch, [
-        (lambda i: (lambda: dptq.rotate_quant_fp6(xs[i % R], h, a6, s6)))(i) for i in range(reps)]) / 1e3
-    out["gemm_fp6_a4"] = _graph_time(torch, [
-        (lambda i: (lambda: dptq.qlinear_fp6(a6, s6, w6s[i % R], ws, M, K, N, y)))(i)
-        for i in range(reps)]) / 1e3
-    # the int8 matrix-core kernels for both precisions: the step's A8 GEMM on
-    # weights in the 8-bit activation order, and for comparison the A8 and A4
-    # GEMMs on the canonical nibble order
-    for bits in (8, 4):
-        codes, scales = dptq.rotate_quant(x, h, bits)
-        if bits == 8:
-            out["gemm_a8"] = _graph_time(torch, [
-                (lambda i: (lambda: dptq.qlinear_a8(codes, scales, w8s[i % R], ws, y)))(i)
-                for i in range(reps)]) / 1e3
-        out[f"gemm_a{bits}_canonical_order"] = _graph_time(torch, [
-            (lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
-            for i in range(reps)]) / 1e3
-        out[f"rotate_quant_a{bits}"] = _graph_time(torch, [
-            (lambda i: (lambda: dptq.rotate_quant(xs[i % R], h, bits, codes, scales)))(i)
-            for i in range(reps)]) / 1e3
-    return out
-
-
-def _graph_time(torch, fns, reps=5):
+def graph_time(torch, fns, reps=5):
     """Microseconds per call of a sequence of launches, captured once in a HIP
-    graph and replayed (no host launch gaps)."""
+    graph and replayed `reps` times between two HIP events on the launch
+    stream (no host launch gaps)."""
     for f in fns:
         f()
     torch.cuda.synchronize()
@@ -274,372 +151,645 @@ def _graph_time(torch, fns, reps=5):
             f()
     g.replay()
     torch.cuda.synchronize()
-    e0, e1 = _events(torch, 2)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(reps):
         g.replay()
     e1.record()
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) * 1e3 / (reps * len(fns))
+    us = e0.elapsed_time(e1) * 1e3 / (reps * len(fns))
+    del g
+    return us
 
 
-def time_decode(torch, dptq, args):
-    """Decode shapes of the LLaMA-3-8B down projection (K = 14336, N = 4096,
-    h = 28 x 512): GEMM GB/s and rotate+quantize latency, each as graph-replayed
-    back-to-back launches cycling 12 weight copies (more than the 256 MiB
-    last-level cache holds)."""
-    import numpy as np
-    import workloads
-    dev = torch.device("cuda:0")
-    K, N, h = 14336, 4096, 28 * 512
-    rng = np.random.default_rng(2)
-    w = torch.from_numpy(workloads.weights(rng, N, K)).to(dev)
-    wp, ws = dptq.prepare_weights(w, h)
-    del w
-    R = 12
-    wps = [wp.clone() for _ in range(R)]
-    out = {}
-    for M in (1, 4, 16):
-        x = torch.from_numpy(workloads.student_t(rng, M, K)).to(dev)
-        for bits in (4, 8):
-            codes, scales = dptq.rotate_quant(x, h, bits)
-            y = torch.empty((M, N), dtype=torch.float16, device=dev)
-            us = _graph_time(torch, [
-                (lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
-                for i in range(24)])
-            nbytes = N * K // 2 + 4 * N + M * K * bits // 8 + 4 * M + 2 * M * N
-            out[f"decode_M{M}_a{bits}"] = {"us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
-            us_rq = _graph_time(torch, [lambda: dptq.rotate_quant(x, h, bits, codes, scales)] * 24)
-            out[f"rotate_quant_M{M}_a{bits}_us"] = round(us_rq, 2)
-    return out
+def k1_bytes(M, K, bits):
+    """Algorithmic bytes of rotate+quantize: fp16 rows in, codes and scales out."""
+    return 2 * M * K + M * K * bits // 8 + 4 * M
 
 
-def time_decode_fused(torch, dptq):
-    """Decode from fp16 x (rotate + quantize + GEMM) on both paths of the
-    fused entry point and on its automatic choice, at LLaMA decode shapes:
-    graph-replayed launches cycling weight copies beyond the last-level cache.
-    GB/s counts the weights, their scales, x, the codes written and y."""
-    import numpy as np
-    import workloads
-    dev = torch.device("cuda:0")
-    shapes = [("llama2_7b_qkv", 1, 4096, 12288, 4096), ("llama2_7b_qkv", 2, 4096, 12288, 4096),
-              ("llama2_7b_o", 1, 4096, 4096, 4096), ("llama2_7b_down", 1, 11008, 4096, 256),
-              ("llama3_8b_down", 1, 14336, 4096, 28 * 512), ("llama3_8b_down", 4, 14336, 4096, 28 * 512),
-              ("llama3_8b_down", 16, 14336, 4096, 28 * 512), ("llama2_70b_qkv", 8, 8192, 10240, 8192)]
-    modes = {"auto": dptq.DECODE_AUTO, "one_launch": dptq.DECODE_ONE_LAUNCH,
-             "two_launches": dptq.DECODE_TWO_LAUNCHES}
-    rng = np.random.default_rng(6)
-    out = {}
-    for name, M, K, N, h in shapes:
-        R = max(2, (300 << 20) // (N * K // 2))
+def gemm_bytes(M, K, N, bits):
+    """Algorithmic bytes of the GEMM: codes, 4-bit weights, scales and fp16 y."""
+    return M * K * bits // 8 + N * K // 2 + 4 * (M + N) + 2 * M * N
+
+
+# ---------------------------------------------------------------------------
+# the headline stack
+# ---------------------------------------------------------------------------
+class Stack:
+    """Every linear of a layer stack with its own weights on the device.
+
+    Weights: N(0, 0.02) fp32 drawn on the device per (layer, linear) with a
+    seeded generator, quantized by dptq.prepare_weights (Eq. 5, per-channel
+    4-bit) and pre-packed into the layout of the GEMM that runs the layer's
+    bits: FP6 for a 4-bit layer, the 8-bit activation order for an 8-bit one.
+    `fp6_all` / `a8_all` pack every layer into that layout as well (to run
+    other policies on the same weights); `canonical` keeps the canonical codes
+    (for decode)."""
+
+    def __init__(self, torch, dptq, name, M, bits, fp6_all=False, a8_all=False, canonical=False):
+        import workloads
+        self.torch, self.dptq = torch, dptq
+        dev = torch.device("cuda:0")
+        cfg = workloads.CONFIGS[name]
+        self.name, self.M, self.L, self.lins = name, M, cfg["L"], cfg["linears"]
+        self.bits = list(bits)
         gen = torch.Generator(device=dev)
-        gen.manual_seed(M + K + N)
-        wps = [torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen)
-               for _ in range(R)]
-        ws = torch.from_numpy(workloads.random_scales(rng, N)).to(dev)
-        x = torch.from_numpy(workloads.student_t(rng, M, K)).to(dev)
-        y = torch.empty((M, N), dtype=torch.float16, device=dev)
-        for bits in (4, 8):
-            codes, scales = dptq.rotate_quant(x, h, bits)
-            nbytes = N * K // 2 + 4 * N + 2 * M * K + M * K * bits // 8 + 4 * M + 2 * M * N
-            rec = {}
-            for mname, mode in modes.items():
-                try:
-                    us = _graph_time(torch, [
-                        (lambda i, mode=mode: (lambda: dptq.qlinear_decode_fused(
-                            x, h, bits, wps[i % R], ws, y, codes, scales, mode=mode)))(i)
-                        for i in range(24)])
-                except dptq.DptqError:
-                    continue          # the rows do not fit on chip for one launch
-                rec[mname] = {"us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
-            out[f"{name}_M{M}_a{bits}"] = rec
-        del wps
-        torch.cuda.empty_cache()
-    return out
+        self.fp6, self.a8, self.canon, self.ws = [], [], [], []
+        for l in range(self.L):
+            f6, a8, can, wsl = [], [], [], []
+            for i, (_, K, N, h) in enumerate(self.lins):
+                gen.manual_seed(cfg["seed"] * 1000003 + l * 16 + i)
+                w = torch.randn((N, K), device=dev, generator=gen, dtype=torch.float32)
+                w.mul_(0.02)
+                wp, ws = dptq.prepare_weights(w, h)
+                del w
+                b = self.bits[l]
+                f6.append(dptq.prepack_weights(wp, dptq.WEIGHTS_FP6) if fp6_all or b == 4 else None)
+                a8.append(dptq.prepack_weights(wp, dptq.WEIGHTS_A8_ORDER).view(N, K // 2)
+                          if a8_all or b == 8 else None)
+                can.append(wp if canonical else None)
+                wsl.append(ws)
+                del wp
+            self.fp6.append(f6)
+            self.a8.append(a8)
+            self.canon.append(can)
+            self.ws.append(wsl)
+        self.X = [torch.from_numpy(workloads.stack_layer_input(name, self.L // 2, n, M=M)).to(dev)
+                  for n, *_ in self.lins]
+        Kmax = max(K for _, K, _, _ in self.lins)
+        Nmax = max(N for _, _, N, _ in self.lins)
+        self.cbuf = torch.empty(M * Kmax, dtype=torch.int8, device=dev)
+        self.a6buf = torch.empty(dptq.fp6_bytes(M, Kmax), dtype=torch.uint8, device=dev)
+        self.sbuf = torch.empty(M, dtype=torch.float32, device=dev)
+        self.ybuf = torch.empty(M * Nmax, dtype=torch.float16, device=dev)
+        self.f6bytes = {K: dptq.fp6_bytes(M, K) for _, K, _, _ in self.lins}
+        torch.cuda.synchronize()
+
+    def ops(self):
+        return 2.0 * self.M * sum(K * N for _, K, N, _ in self.lins) * self.L
+
+    def weight_bytes(self):
+        return sum(N * K // 2 + 4 * N for _, K, N, _ in self.lins) * self.L
+
+    def launches(self, bits, events=None):
+        """One pass over every linear: rotate+quantize then GEMM per linear.
+        With `events`, a HIP event pair is recorded around every launch and
+        (kernel, linear, start, end) appended."""
+        dptq, M = self.dptq, self.M
+        for l in range(self.L):
+            b = bits[l]
+            for i, (lin, K, N, h) in enumerate(self.lins):
+                y = self.ybuf[: M * N].view(M, N)
+                if b == 4:
+                    a6 = self.a6buf[: self.f6bytes[K]]
+                    k1 = lambda: dptq.rotate_quant_fp6(self.X[i], h, a6, self.sbuf)
+                    g = lambda: dptq.qlinear_fp6(a6, self.sbuf, self.fp6[l][i], self.ws[l][i], M, K, N, y)
+                    names = ("rq_fp6_a4", "gemm_fp6_a4")
+                else:
+                    codes = self.cbuf[: M * K].view(M, K)
+                    k1 = lambda: dptq.rotate_quant(self.X[i], h, 8, codes, self.sbuf)
+                    g = lambda: dptq.qlinear_a8(codes, self.sbuf, self.a8[l][i], self.ws[l][i], y)
+                    names = ("rq_a8", "gemm_a8")
+                for kname, f in zip(names, (k1, g)):
+                    if events is None:
+                        f()
+                    else:
+                        e0 = self.torch.cuda.Event(enable_timing=True)
+                        e1 = self.torch.cuda.Event(enable_timing=True)
+                        e0.record()
+                        f()
+                        e1.record()
+                        events.append((kname, lin, e0, e1))
+
+    def decode_launches(self, bits, X):
+        """One pass at decode size: every linear through the decode entry point
+        from fp16 x (its automatic choice of one launch or two), on the
+        canonical weights."""
+        dptq = self.dptq
+        M = X[0].shape[0]
+        for l in range(self.L):
+            b = bits[l]
+            for i, (_, K, N, h) in enumerate(self.lins):
+                dt = self.torch.uint8 if b == 4 else self.torch.int8
+                codes = self.cbuf[: M * K * b // 8].view(dt).view(M, K * b // 8)
+                y = self.ybuf[: M * N].view(M, N)
+                dptq.qlinear_decode_fused(X[i], h, b, self.canon[l][i], self.ws[l][i], y, codes,
+                                          self.sbuf[:M], mode=dptq.DECODE_AUTO)
 
 
-def time_range(torch, dptq, cfg):
-    """The range quantizer variant (Eq. 1 with a zero point) at the step's
-    shape, next to the symmetric path: rotate + quantize, and the linear (the
-    zero-point correction in the GEMM epilogue), each timed over 24
-    graph-replayed launches."""
-    import numpy as np
+def time_headline(torch, dptq, args):
     import workloads
-    dev = torch.device("cuda:0")
-    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
-    rng = np.random.default_rng(7)
-    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
-    wp = torch.from_numpy(workloads.random_weight_bytes(rng, N, K)).to(dev)
-    ws = torch.from_numpy(workloads.random_scales(rng, N)).to(dev)
-    sums = dptq.weight_sums(wp)
-    y = torch.empty((M, N), dtype=torch.float16, device=dev)
-    out = {"weight_sums_us": round(_graph_time(torch, [lambda: dptq.weight_sums(wp, sums)] * 24), 2)}
-    for bits in (4, 8):
-        c, s = dptq.rotate_quant(x, h, bits)
-        cr, sr, zr = dptq.rotate_quant_range(x, h, bits)
-        out[f"a{bits}"] = {
-            "rotate_quant_us": round(_graph_time(torch, [lambda: dptq.rotate_quant(x, h, bits, c, s)] * 24), 2),
-            "rotate_quant_range_us": round(_graph_time(
-                torch, [lambda: dptq.rotate_quant_range(x, h, bits, cr, sr, zr)] * 24), 2),
-            "qlinear_us": round(_graph_time(torch, [lambda: dptq.qlinear(c, s, bits, wp, ws, y)] * 24), 2),
-            "qlinear_range_us": round(_graph_time(
-                torch, [lambda: dptq.qlinear_range(cr, sr, zr, bits, wp, ws, sums, y)] * 24), 2),
-        }
-    return out
+    cfg = workloads.CONFIGS[HEADLINE]
+    L, M = cfg["L"], cfg["M"]
+    mask = workloads.layer_mask(L, 4, cfg["mask_seed"])
+    policy = lambda: dptq.layer_policy(L, mask)          # a1: host lookup, every step
+    t0 = time.perf_counter()
+    st = Stack(torch, dptq, HEADLINE, M, policy(), fp6_all=True, canonical=True)
+    setup_s = time.perf_counter() - t0
+    progress(f"headline stack ready ({setup_s:.1f} s)")
+
+    for _ in range(args.warmup):
+        st.launches(policy())
+    torch.cuda.synchronize()
+    with ClockSampler() as clocks:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record()
+        for _ in range(args.steps):
+            st.launches(policy())
+        e1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    gpu_ms = e0.elapsed_time(e1) / args.steps
+    progress(f"headline: {args.steps} steps, {wall * 1e3 / args.steps:.2f} ms per step")
+
+    # One more step with an event pair around every launch: per-kernel
+    # durations in the step's own order and cache state.
+    events = []
+    st.launches(policy(), events)
+    torch.cuda.synchronize()
+    per = {}
+    for kname, lin, a, b in events:
+        per.setdefault((kname, lin), []).append(a.elapsed_time(b) * 1e3)
+
+    # The same stack with every layer at 4 bits, for the policy's cost.
+    all4 = [4] * L
+    st.launches(all4)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        st.launches(all4)
+    torch.cuda.synchronize()
+    all4_ms = (time.perf_counter() - t0) * 1e3 / 3
+    return st, dict(wall=wall, gpu_ms=gpu_ms, per=per, clocks=clocks.summary(), setup_s=setup_s,
+                    all4_ms=all4_ms, mask=[int(v) for v in mask], bits=policy())
 
 
-def time_calibration(torch, dptq):
-    """Residual-dynamics calibration (Eq. 8-11) of one 4096-wide layer over a
-    2048-token batch: per-token JR and SNR plus the layer means, graph-replayed
-    over 12 input copies; GB/s counts reading x and dx once and writing the
-    statistics."""
+def headline_record(st, r, args):
+    M, L = st.M, st.L
+    ops = st.ops()
+    ms = r["wall"] * 1e3 / args.steps
+    value = ops / (ms * 1e-3) / 1e12
+    lin = {n: (K, N, h) for n, K, N, h in st.lins}
+    bits = r["bits"]
+    n8 = sum(1 for b in bits if b == 8)
+    # per kernel family: launches and time per step, algorithmic work
+    fam = {}
+    kernels = {}
+    for (kname, ln), us in sorted(r["per"].items()):
+        K, N, h = lin[ln]
+        b = 8 if kname.endswith("a8") else 4
+        avg = sum(us) / len(us)
+        ent = {"us": round(avg, 2), "launches_per_step": len(us)}
+        if kname.startswith("gemm"):
+            work = 2.0 * M * N * K
+            ent["TOPS"] = round(work / (avg * 1e-6) / 1e12, 1)
+            ent["frac_of_int8_peak"] = round(ent["TOPS"] / PEAK_INT8_TOPS, 4)
+            if "fp6" in kname:
+                ent["frac_of_fp6_peak"] = round(ent["TOPS"] / PEAK_FP6_TOPS, 4)
+        else:
+            work = k1_bytes(M, K, b)
+            ent["GB/s"] = round(work / (avg * 1e-6) / 1e9, 1)
+            ent["frac_of_hbm_peak"] = round(ent["GB/s"] / PEAK_HBM_GBS, 4)
+        kernels[f"{kname}/{ln}"] = ent
+        f = fam.setdefault(kname, {"us": 0.0, "n": 0, "work": 0.0})
+        f["us"] += sum(us)
+        f["n"] += len(us)
+        f["work"] += work * len(us)
+    dominant = max(fam, key=lambda k: fam[k]["us"])
+    d = fam[dominant]
+    kernel_names = {"gemm_fp6_a4": ("qgemm_fp6<false, false>", PEAK_FP6_TOPS),
+                    "gemm_a8": ("qgemm_prefill_wide<8, false, true, false>", PEAK_INT8_TOPS)}
+    if dominant.startswith("gemm"):
+        kname, peak = kernel_names[dominant]
+        achieved = d["work"] / (d["us"] * 1e-6) / 1e12
+        traffic = measured_traffic() if dominant == "gemm_fp6_a4" else None
+        roof = {"bound": "mfma", "kernel": kname, "achieved": round(achieved, 1), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "frac_of_int8_peak": round(achieved / PEAK_INT8_TOPS, 4),
+                "avg_launch_us": round(d["us"] / d["n"], 2), "launches_per_step": d["n"],
+                "traffic": traffic,
+                "algorithmic_bytes_per_launch": int(sum(
+                    gemm_bytes(M, K, N, 4) for K, N, _ in lin.values()) / len(lin)),
+                "share_of_step": round(d["us"] / 1e3 / ms, 3)}
+    else:
+        achieved = d["work"] / (d["us"] * 1e-6) / 1e9
+        roof = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": None}
+    gemm_us = sum(f["us"] for k, f in fam.items() if k.startswith("gemm"))
+    k1_us = sum(f["us"] for k, f in fam.items() if not k.startswith("gemm"))
+    return value, ms, roof, kernels, {
+        "gemm_ms_per_step": round(gemm_us / 1e3, 3), "rotate_quant_ms_per_step": round(k1_us / 1e3, 3),
+        "gemm_TOPS": round(ops / (gemm_us * 1e-6) / 1e12, 1),
+        "layers_a8": n8, "mask_seed": 5,
+        "all_a4_ms_per_step": round(r["all4_ms"], 3),
+        "mixed_over_all_a4": round(ms / r["all4_ms"], 4),
+    }
+
+
+# ---------------------------------------------------------------------------
+# other workloads (graph-replayed)
+# ---------------------------------------------------------------------------
+def single_linear(torch, dptq, name, M, copies_bytes=300 << 20):
+    """K1 and GEMM of one linear at 4 bits (FP6 path and int8 path) and at 8
+    bits (8-bit-order weights), inputs and weights cycling through copies
+    beyond the last-level cache."""
     import numpy as np
-    import workloads
-    dev = torch.device("cuda:0")
-    T, K, h = 2048, 4096, 4096
-    x, dx = workloads.residual_stream(np.random.default_rng(11), 2, T, K)[0]
-    R = 12
-    xs = [torch.from_numpy(x).to(dev) for _ in range(R)]
-    dxs = [torch.from_numpy(dx).to(dev) for _ in range(R)]
-    jr = torch.empty(T, dtype=torch.float32, device=dev)
-    snr = torch.empty(T, dtype=torch.float32, device=dev)
-    means = torch.empty(2, dtype=torch.float64, device=dev)
-    out = {}
-    for bits in (4, 8):
-        us = _graph_time(torch, [
-            (lambda i: (lambda: dptq.residual_dynamics(xs[i % R], dxs[i % R], h, bits,
-                                                       jr=jr, snr=snr, means=means)))(i)
-            for i in range(24)])
-        nbytes = 2 * 2 * T * K + 8 * T + 16
-        out[f"residual_dynamics_a{bits}"] = {"us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
-    return out
-
-
-def time_kv(torch, dptq):
-    """Group-wise KV4 codec on one layer's keys of a 32-sequence x 2048-token
-    prefill for LLaMA-3-8B (8 KV heads x 128 = 1024 per token, group 128):
-    quantize and reconstruct, graph-replayed over 4 distinct caches (> 256 MiB
-    each way).  Algorithmic bytes: 2 B in, 0.5 B of codes and 8 B of (s, m)
-    per 128-element group out, and the reverse for the reconstruction."""
-    import numpy as np
-    dev = torch.device("cuda:0")
-    T, D, g = 32 * 2048, 1024, 128
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(8)
-    R = 4
-    xs = [torch.randn((T, D), device=dev, generator=gen).half() for _ in range(R)]
-    outs = [dptq.kv_quant(x, g) for x in xs]
-    rec = [torch.empty((T, D), dtype=torch.float16, device=dev) for _ in range(R)]
-    nbytes = 2 * T * D + T * D // 2 + 8 * T * (D // g)
-    q_us = _graph_time(torch, [
-        (lambda i: (lambda: dptq.kv_quant(xs[i % R], g, *outs[i % R])))(i) for i in range(8)])
-    d_us = _graph_time(torch, [
-        (lambda i: (lambda: dptq.kv_dequant(*outs[i % R], g, out=rec[i % R])))(i) for i in range(8)])
-    del xs, outs, rec
-    torch.cuda.empty_cache()
-    return {"tokens": T, "row": D, "group": g,
-            "quant_us": round(q_us, 2), "quant_GB/s": round(nbytes / q_us / 1e3, 1),
-            "dequant_us": round(d_us, 2), "dequant_GB/s": round(nbytes / d_us / 1e3, 1)}
-
-
-def time_stack(torch, dptq, name, Ms, reps=3):
-    """End-to-end time of every linear of a whole layer stack (rotate+quantize
-    and GEMM per linear, layer bits from the policy), captured as one HIP graph
-    per policy and replayed.  Each layer has its own weights (random packed
-    code bytes drawn on the device: the time does not depend on their values);
-    each linear's input is the seeded stack input of a mid-stack layer.  At
-    decode sizes (M <= 16) each linear is one call of the decode entry point,
-    which picks one launch or two.
-    Returns ms per stack for all-4-bit, the paper's default set, a seeded
-    4-layer mask and all-8-bit activations, and the mixed/all-4-bit ratios.
-    At prefill sizes the same policies run again with the 4-bit layers on the
-    FP6 path (rotate+quantize into the FP6 layout, FP6 GEMM against weights
-    packed once into it) and the 8-bit layers on the int8 path against weights
-    packed once into the 8-bit activation order: the "_fp6" entries."""
     import workloads
     dev = torch.device("cuda:0")
     cfg = workloads.CONFIGS[name]
-    L, lins = cfg["L"], cfg["linears"]
+    K, N, h = cfg["K"], cfg["N"], cfg["h"]
+    x = torch.from_numpy(workloads.activations_for(name, M=M)).to(dev)
     gen = torch.Generator(device=dev)
-    gen.manual_seed(cfg["seed"])
-    W = [[(torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen),
-           torch.rand(N, device=dev, generator=gen) * 1e-3 + 1e-4)
-          for _, K, N, _ in lins] for _ in range(L)]
-    wbytes = sum(N * K // 2 + 4 * N for _, K, N, _ in lins) * L
-    policies = {"all_a4": [4] * L, "default": dptq.layer_policy(L),
-                "seeded_mask": dptq.layer_policy(L, workloads.layer_mask(L, 4, cfg["mask_seed"])),
-                "all_a8": [8] * L}
-    out = {"weights_GB": round(wbytes / 1e9, 2)}
-    W6 = W8 = None
-    if any(M > 16 for M in Ms):
-        W6 = [[dptq.pack_fp6(W[l][i][0]) for i in range(len(lins))] for l in range(L)]
-        W8 = [[dptq.pack_w4_a8(W[l][i][0]) for i in range(len(lins))] for l in range(L)]
-    for M in Ms:
-        X = [torch.from_numpy(workloads.stack_layer_input(name, L // 2, n, M=M)).to(dev)
-             for n, *_ in lins]
-        Kmax = max(K for _, K, _, _ in lins)
-        Nmax = max(N for _, _, N, _ in lins)
-        cbuf = torch.empty(M * Kmax, dtype=torch.uint8, device=dev)
-        sbuf = torch.empty(M, dtype=torch.float32, device=dev)
-        ybuf = torch.empty(M * Nmax, dtype=torch.float16, device=dev)
-        res = {}
-        for pname, bits in policies.items():
-            def run(bits=bits):
-                for l in range(L):
-                    b = bits[l]
-                    for i, (_, K, N, h) in enumerate(lins):
-                        dt = torch.uint8 if b == 4 else torch.int8
-                        codes = cbuf[: M * K * b // 8].view(dt).view(M, K * b // 8)
-                        y = ybuf[: M * N].view(M, N)
-                        if M <= 16:   # the decode entry point's own choice of path
-                            dptq.qlinear_decode_fused(X[i], h, b, W[l][i][0], W[l][i][1], y, codes,
-                                                      sbuf, mode=dptq.DECODE_AUTO)
-                        else:
-                            dptq.rotate_quant(X[i], h, b, codes, sbuf)
-                            dptq.qlinear(codes, sbuf, b, W[l][i][0], W[l][i][1], y)
-            res[pname] = _graph_time(torch, [run], reps=reps) / 1e3
-        if M > 16:
-            a6buf = torch.empty(max(dptq.fp6_bytes(M, K) for _, K, _, _ in lins), dtype=torch.uint8,
-                                device=dev)
-            for pname in ("all_a4", "default", "seeded_mask"):
-                bits = policies[pname]
+    gen.manual_seed(cfg["seed"] + 17)
+    w = torch.randn((N, K), device=dev, generator=gen) * 0.02
+    wp, ws = dptq.prepare_weights(w, h)
+    del w
+    R = int(max(2, min(16, copies_bytes // max(1, N * K // 2 + 2 * M * K))))
+    xs = [x.clone() for _ in range(R)]
+    wps = [wp.clone() for _ in range(R)]
+    w6s = [dptq.prepack_weights(wp, dptq.WEIGHTS_FP6) for _ in range(R)] \
+        if K % 128 == 0 and M > 16 else None
+    w8s = [dptq.prepack_weights(wp, dptq.WEIGHTS_A8_ORDER).view(N, K // 2) for _ in range(R)] \
+        if K % 128 == 0 else None
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
+    out = {"M": M, "K": K, "N": N, "had_size": h}
+    n = 24
+    ops = 2.0 * M * N * K
 
-                def run6(bits=bits):
-                    for l in range(L):
-                        b = bits[l]
-                        for i, (_, K, N, h) in enumerate(lins):
-                            y = ybuf[: M * N].view(M, N)
-                            if b == 4:
-                                a6 = a6buf[: dptq.fp6_bytes(M, K)]
-                                dptq.rotate_quant_fp6(X[i], h, a6, sbuf)
-                                dptq.qlinear_fp6(a6, sbuf, W6[l][i], W[l][i][1], M, K, N, y)
-                            else:
-                                codes = cbuf[: M * K].view(torch.int8).view(M, K)
-                                dptq.rotate_quant(X[i], h, 8, codes, sbuf)
-                                dptq.qlinear_a8(codes, sbuf, W8[l][i], W[l][i][1], y)
-                res[pname + "_fp6"] = _graph_time(torch, [run6], reps=reps) / 1e3
-            del a6buf
-        ops = 2.0 * M * sum(K * N for _, K, N, _ in lins) * L
-        ent = {f"{p}_ms": round(v, 3) for p, v in res.items()}
-        ent["default_over_all_a4"] = round(res["default"] / res["all_a4"], 4)
-        ent["seeded_mask_over_all_a4"] = round(res["seeded_mask"] / res["all_a4"], 4)
-        ent["all_a4_TOPS"] = round(ops / (res["all_a4"] * 1e-3) / 1e12, 1)
-        ent["all_a4_weight_GB/s"] = round(wbytes / (res["all_a4"] * 1e-3) / 1e9, 1)
-        if "all_a4_fp6" in res:
-            ent["default_fp6_over_all_a4_fp6"] = round(res["default_fp6"] / res["all_a4_fp6"], 4)
-            ent["seeded_mask_fp6_over_all_a4_fp6"] = round(res["seeded_mask_fp6"] / res["all_a4_fp6"], 4)
-            ent["all_a4_fp6_TOPS"] = round(ops / (res["all_a4_fp6"] * 1e-3) / 1e12, 1)
-        out[f"M{M}"] = ent
-        del X, cbuf, ybuf
-    del W, W6, W8
+    def rec(k1_us, g_us, bits, path):
+        r = {"rotate_quant_us": round(k1_us, 2), "gemm_us": round(g_us, 2),
+             "rotate_quant_GB/s": round(k1_bytes(M, K, bits) / (k1_us * 1e-6) / 1e9, 1),
+             "qlinear_TOPS": round(ops / ((k1_us + g_us) * 1e-6) / 1e12, 2),
+             "gemm_TOPS": round(ops / (g_us * 1e-6) / 1e12, 2),
+             "gemm_frac_of_int8_peak": round(ops / (g_us * 1e-6) / 1e12 / PEAK_INT8_TOPS, 4)}
+        if path == "fp6":
+            r["gemm_frac_of_fp6_peak"] = round(ops / (g_us * 1e-6) / 1e12 / PEAK_FP6_TOPS, 4)
+        if M <= 16:
+            r["gemm_GB/s"] = round(gemm_bytes(M, K, N, bits) / (g_us * 1e-6) / 1e9, 1)
+            r["gemm_frac_of_hbm_peak"] = round(r["gemm_GB/s"] / PEAK_HBM_GBS, 4)
+        return r
+
+    for bits in (4, 8):
+        codes, scales = dptq.rotate_quant(x, h, bits)
+        k1 = graph_time(torch, [(lambda i: (lambda: dptq.rotate_quant(xs[i % R], h, bits, codes, scales)))(i)
+                                for i in range(n)])
+        g = graph_time(torch, [(lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
+                               for i in range(n)])
+        out[f"a{bits}_int8"] = rec(k1, g, bits, "int8")
+        if bits == 8 and w8s is not None:
+            g8 = graph_time(torch, [(lambda i: (lambda: dptq.qlinear_a8(codes, scales, w8s[i % R], ws, y)))(i)
+                                    for i in range(n)])
+            out["a8_int8_a8order"] = rec(k1, g8, 8, "int8")
+        if bits == 4 and w6s is not None and M > 16:   # the FP6 path serves prefill sizes
+            a6, s6 = dptq.rotate_quant_fp6(x, h)
+            k16 = graph_time(torch, [(lambda i: (lambda: dptq.rotate_quant_fp6(xs[i % R], h, a6, s6)))(i)
+                                     for i in range(n)])
+            g6 = graph_time(torch, [(lambda i: (lambda: dptq.qlinear_fp6(a6, s6, w6s[i % R], ws, M, K, N, y)))(i)
+                                    for i in range(n)])
+            out["a4_fp6"] = rec(k16, g6, 4, "fp6")
+            # the FP6 layout's output bytes are 0.75 per code; GB/s above counts
+            # the algorithmic 0.5
+        if M <= 16:
+            d = graph_time(torch, [(lambda i: (lambda: dptq.qlinear_decode_fused(
+                x, h, bits, wps[i % R], ws, y, codes, scales, mode=dptq.DECODE_AUTO)))(i) for i in range(n)])
+            out[f"a{bits}_decode_from_x_us"] = round(d, 2)
+    del xs, wps, w6s, w8s
     torch.cuda.empty_cache()
     return out
 
 
-def cpu_baseline(cfg, rows, seed=123):
-    """Time the CPU oracle on a bounded sample: `rows` token rows of the same
-    layer, both precisions (rotation + quantization + exact GEMM + epilogue)."""
+def stack_7b(torch, dptq):
+    """The LLaMA-2-7B 32-layer linear stack at M = 2048: the seeded 4-of-32
+    mask, the paper's default set and all-4-bit, each one graph replay."""
+    import workloads
+    cfg = workloads.CONFIGS["llama2_7b_stack"]
+    L, M = cfg["L"], cfg["M"]
+    pol = {"seeded_mask": dptq.layer_policy(L, workloads.layer_mask(L, 4, cfg["mask_seed"])),
+           "paper_default": dptq.layer_policy(L), "all_a4": [4] * L}
+    st = Stack(torch, dptq, "llama2_7b_stack", M, pol["seeded_mask"], fp6_all=True, a8_all=True)
+    out = {"M": M, "layers": L, "weights_GB": round(st.weight_bytes() / 1e9, 2)}
+    res = {p: graph_time(torch, [lambda bits=bits: st.launches(bits)], reps=2) / 1e3
+           for p, bits in pol.items()}
+    ops = st.ops()
+    for p, ms in res.items():
+        out[f"{p}_ms"] = round(ms, 3)
+        out[f"{p}_TOPS"] = round(ops / (ms * 1e-3) / 1e12, 1)
+    out["seeded_mask_over_all_a4"] = round(res["seeded_mask"] / res["all_a4"], 4)
+    out["paper_default_over_all_a4"] = round(res["paper_default"] / res["all_a4"], 4)
+    del st
+    torch.cuda.empty_cache()
+    return out
+
+
+def decode_70b(torch, st, bits):
+    """The headline stack at M = 8 decode (every linear from fp16 x through the
+    decode entry point), one graph replay per pass."""
+    import workloads
+    dev = torch.device("cuda:0")
+    X = [torch.from_numpy(workloads.stack_layer_input(HEADLINE, st.L // 2, n, M=8)).to(dev)
+         for n, *_ in st.lins]
+    ms = graph_time(torch, [lambda: st.decode_launches(bits, X)], reps=3) / 1e3
+    return {"M": 8, "layers": st.L, "ms": round(ms, 3),
+            "weight_GB/s": round(st.weight_bytes() / (ms * 1e-3) / 1e9, 1),
+            "frac_of_hbm_peak": round(st.weight_bytes() / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
+def time_extended(torch, dptq):
+    """Variants outside the headline: the range quantizer, calibration, KV4."""
     import numpy as np
     import workloads
-    from oracle import rotate_quant_ref, qlinear_ref
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    except Exception:
-        blas_threads = 1
-    M, K, N, h = cfg["M"], cfg["K"], cfg["N"], cfg["h"]
-    rng = np.random.default_rng(seed)
-    x = workloads.gauss_outliers(rng, rows, K)
-    wp = workloads.random_weight_bytes(rng, N, K)
-    ws = workloads.random_scales(rng, N)
-    t0 = time.perf_counter()
+    dev = torch.device("cuda:0")
+    out = {}
+    M, K, N, h = 2048, 4096, 12288, 4096
+    rng = np.random.default_rng(7)
+    x = torch.from_numpy(workloads.gauss_outliers(rng, M, K)).to(dev)
+    wp = torch.from_numpy(workloads.random_weight_bytes(rng, N, K)).to(dev)
+    ws = torch.full((N,), 1e-5, device=dev)
+    sums = dptq.weight_sums(wp)
+    y = torch.empty((M, N), dtype=torch.float16, device=dev)
     for bits in (4, 8):
-        c, s = rotate_quant_ref(x, h, bits)
-        qlinear_ref(c, s, bits, wp, ws)
-    dt = time.perf_counter() - t0
-    ops = 2 * (2.0 * rows * N * K)
-    return {"value": round(ops / dt / 1e12, 6), "unit": "TOPS", "cores": int(blas_threads),
-            "kind": "oracle",
-            "sample": f"{rows} of {M} token rows, A4 and A8, K={K}, N={N}, h={h}: "
-                      f"rotation, quantization, exact GEMM and epilogue; {dt:.1f} s"}
+        cr, sr, zr = dptq.rotate_quant_range(x, h, bits)
+        out[f"range_a{bits}"] = {
+            "rotate_quant_range_us": round(graph_time(
+                torch, [lambda: dptq.rotate_quant_range(x, h, bits, cr, sr, zr)] * 24), 2),
+            "qlinear_range_us": round(graph_time(
+                torch, [lambda: dptq.qlinear_range(cr, sr, zr, bits, wp, ws, sums, y)] * 24), 2)}
+    T = 2048
+    xs, dxs = workloads.residual_stream(np.random.default_rng(11), 2, T, K)[0]
+    xd, dxd = torch.from_numpy(xs).to(dev), torch.from_numpy(dxs).to(dev)
+    jr = torch.empty(T, dtype=torch.float32, device=dev)
+    snr = torch.empty(T, dtype=torch.float32, device=dev)
+    means = torch.empty(2, dtype=torch.float64, device=dev)
+    for bits in (4, 8):
+        us = graph_time(torch, [lambda: dptq.residual_dynamics(xd, dxd, h, bits, jr=jr, snr=snr,
+                                                               means=means)] * 24)
+        out[f"calibration_a{bits}"] = {"us": round(us, 2),
+                                       "GB/s": round((4 * T * K + 8 * T) / (us * 1e-6) / 1e9, 1)}
+    T, D, g = 32 * 2048, 1024, 128
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(8)
+    kv = [torch.randn((T, D), device=dev, generator=gen).half() for _ in range(4)]
+    outs = [dptq.kv_quant(t, g) for t in kv]
+    rec = [torch.empty((T, D), dtype=torch.float16, device=dev) for _ in range(4)]
+    nb = 2 * T * D + T * D // 2 + 8 * T * (D // g)
+    q = graph_time(torch, [(lambda i: (lambda: dptq.kv_quant(kv[i % 4], g, *outs[i % 4])))(i) for i in range(8)])
+    d = graph_time(torch, [(lambda i: (lambda: dptq.kv_dequant(*outs[i % 4], g, out=rec[i % 4])))(i)
+                           for i in range(8)])
+    out["kv4"] = {"tokens": T, "row": D, "group": g, "quant_us": round(q, 2),
+                  "quant_GB/s": round(nb / (q * 1e-6) / 1e9, 1), "dequant_us": round(d, 2),
+                  "dequant_GB/s": round(nb / (d * 1e-6) / 1e9, 1)}
+    return out
 
 
+# ---------------------------------------------------------------------------
+# counter runs
+# ---------------------------------------------------------------------------
+def run_only(torch, dptq, args):
+    """One kernel family of the headline step at each of its four linear
+    shapes, --steps launches per shape, nothing timed (rocprofv3 --pmc)."""
+    dev = torch.device("cuda:0")
+    if args.only == "copy":
+        n = 256 << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"only": "copy", "bytes_per_launch": n}))
+        return
+    import workloads
+    cfg = workloads.CONFIGS[HEADLINE]
+    M = cfg["M"]
+    bits = 4 if args.only.endswith("6") else 8
+    lins = cfg["linears"]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1)
+    X = [torch.from_numpy(workloads.stack_layer_input(HEADLINE, 40, n, M=M)).to(dev) for n, *_ in lins]
+    W = []
+    for _, K, N, _ in lins:
+        wp = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen)
+        layout = dptq.WEIGHTS_FP6 if bits == 4 else dptq.WEIGHTS_A8_ORDER
+        W.append((dptq.prepack_weights(wp, layout), torch.full((N,), 1e-5, device=dev)))
+        del wp
+    Kmax = max(K for _, K, _, _ in lins)
+    Nmax = max(N for _, _, N, _ in lins)
+    a6 = torch.empty(dptq.fp6_bytes(M, Kmax), dtype=torch.uint8, device=dev)
+    c8 = torch.empty(M * Kmax, dtype=torch.int8, device=dev)
+    s = torch.empty(M, dtype=torch.float32, device=dev)
+    yb = torch.empty(M * Nmax, dtype=torch.float16, device=dev)
+    # valid operands in the shared buffers: the largest linear's codes
+    iK = max(range(len(lins)), key=lambda i: lins[i][1])
+    if bits == 4:
+        dptq.rotate_quant_fp6(X[iK], lins[iK][3], a6[: dptq.fp6_bytes(M, lins[iK][1])], s)
+    else:
+        dptq.rotate_quant(X[iK], lins[iK][3], 8, c8[: M * lins[iK][1]].view(M, -1), s)
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        for i, (_, K, N, h) in enumerate(lins):
+            y = yb[: M * N].view(M, N)
+            if bits == 4:
+                a = a6[: dptq.fp6_bytes(M, K)]
+                if args.only == "rq6":
+                    dptq.rotate_quant_fp6(X[i], h, a, s)
+                else:
+                    dptq.qlinear_fp6(a, s, W[i][0], W[i][1], M, K, N, y)
+            else:
+                c = c8[: M * K].view(M, K)
+                if args.only == "rq8":
+                    dptq.rotate_quant(X[i], h, 8, c, s)
+                else:
+                    dptq.qlinear_a8(c, s, W[i][0].view(N, K // 2), W[i][1], y)
+    torch.cuda.synchronize()
+    print(json.dumps({"only": args.only, "launches_per_shape": args.steps,
+                      "shapes": [[M, K, N] for _, K, N, _ in lins]}))
+
+
+# ---------------------------------------------------------------------------
+# CPU oracle baseline (runs before the GPU is touched)
+# ---------------------------------------------------------------------------
+_JOB = None
+
+
+def _one_thread():
+    try:
+        from threadpoolctl import threadpool_limits
+        threadpool_limits(1)
+    except Exception:
+        pass
+
+
+def _rotate_chunk(rows):
+    """The oracle's rotate+quantize on token rows [rows[0], rows[1]) of the job."""
+    from oracle import rotate_quant_ref
+    x, h, bits = _JOB[:3]
+    return rotate_quant_ref(x[rows[0]:rows[1]], h, bits)
+
+
+def _gemm_chunk(cols):
+    """The oracle's exact GEMM and epilogue for output channels [cols[0], cols[1])."""
+    from oracle import qlinear_ref
+    codes, scales, bits, wq, ws = _JOB
+    return qlinear_ref(codes, scales, bits, wq[cols[0]:cols[1]], ws[cols[0]:cols[1]])
+
+
+def _split(n, parts):
+    k = max(1, min(n, parts))
+    return [(n * i // k, n * (i + 1) // k) for i in range(k) if n * (i + 1) // k > n * i // k]
+
+
+def _oracle_job(P, x, h, bits, wq, ws):
+    """Seconds of the oracle on every row of x over P forked single-threaded
+    workers: rotate+quantize split by token rows, then the exact GEMM and
+    epilogue split by output channels.  Returns (rotate s, GEMM s)."""
+    import multiprocessing as mp
+    import numpy as np
+    global _JOB
+    ctx = mp.get_context("fork")
+    _JOB = (x, h, bits)
+    with ctx.Pool(P, initializer=_one_thread) as pool:
+        t0 = time.perf_counter()
+        parts = pool.map(_rotate_chunk, _split(x.shape[0], P))
+        t_rot = time.perf_counter() - t0
+    codes = np.concatenate([c for c, _ in parts])
+    scales = np.concatenate([s for _, s in parts])
+    _JOB = (codes, scales, bits, wq, ws)
+    with ctx.Pool(P, initializer=_one_thread) as pool:
+        t0 = time.perf_counter()
+        pool.map(_gemm_chunk, _split(wq.shape[0], P))
+        t_gemm = time.perf_counter() - t0
+    _JOB = None
+    return t_rot, t_gemm
+
+
+def cpu_baseline(P):
+    """The oracle timed on the host's cores (Section 4.9 workloads stand-ins):
+    configs 1-3 in full, the two stacks on 256 seeded rows per linear at each
+    bit width, extrapolated linearly in M and over the layers of the mask."""
+    import numpy as np
+    import workloads
+    cores = os.cpu_count()
+    aff = len(os.sched_getaffinity(0))
+    P = P or max(1, min(16, aff))
+    rng = np.random.default_rng(123)
+
+    def weights_for(x, K, N):
+        wq = workloads.random_weight_bytes(rng, N, K)
+        l1 = float(np.max(np.sum(np.abs(x.astype(np.float32)), axis=1))) or 1.0
+        ws = (rng.uniform(0.5, 1.0, N) * 3e4 / (8 * K * l1)).astype(np.float32)
+        return wq, ws
+
+    out = {"cores": cores, "affinity": aff, "workers": P, "configs": {}}
+    t_all = time.perf_counter()
+    singles = [("tiny", 16), ("llama2_7b_qkv", 2048), ("llama3_8b_down", 1), ("llama3_8b_down", 4),
+               ("llama3_8b_down", 16), ("llama3_8b_down", 2048)]
+    for name, M in singles:
+        cfg = workloads.CONFIGS[name]
+        K, N, h = cfg["K"], cfg["N"], cfg["h"]
+        x = workloads.activations_for(name, M=M)
+        wq, ws = weights_for(x, K, N)
+        ent = {}
+        for bits in (4, 8):
+            tr, tg = _oracle_job(P, x, h, bits, wq, ws)
+            ent[f"a{bits}"] = {"rotate_quant_s": round(tr, 3), "gemm_s": round(tg, 3),
+                               "TOPS": round(2.0 * M * N * K / (tr + tg) / 1e12, 6)}
+        out["configs"][f"{name}_M{M}"] = ent
+        progress(f"cpu baseline: {name} M={M} done")
+    for name, mask_seed in (("llama2_7b_stack", 3), (HEADLINE, 5)):
+        cfg = workloads.CONFIGS[name]
+        L, M = cfg["L"], cfg["M"]
+        mask = workloads.layer_mask(L, 4, mask_seed)
+        n8 = int(mask.sum())
+        per_bits = {4: 0.0, 8: 0.0}
+        rows = 256
+        for lin, K, N, h in cfg["linears"]:
+            x = workloads.stack_layer_input(name, L // 2, lin, M=rows)
+            wq, ws = weights_for(x, K, N)
+            for bits in (4, 8):
+                tr, tg = _oracle_job(P, x, h, bits, wq, ws)
+                per_bits[bits] += (tr + tg) * M / rows    # one layer's linears at M tokens
+                progress(f"cpu baseline: {name}/{lin} A{bits} {tr + tg:.1f} s")
+        est = per_bits[4] * (L - n8) + per_bits[8] * n8
+        ops = 2.0 * M * sum(K * N for _, K, N, _ in cfg["linears"]) * L
+        progress(f"cpu baseline: {name} sampled rows done")
+        out["configs"][name] = {"M": M, "layers": L, "sampled_rows_per_linear": rows,
+                                "extrapolated": True, "s": round(est, 1),
+                                "TOPS": round(ops / est / 1e12, 6)}
+    out["total_s"] = round(time.perf_counter() - t_all, 1)
+    head = out["configs"][HEADLINE]
+    return {"value": head["TOPS"], "unit": "TOPS", "cores": P, "kind": "oracle",
+            "sample": (f"{head['sampled_rows_per_linear']} seeded token rows per linear of the "
+                       f"LLaMA-2-70B stack at each bit width (rotation, quantization, exact GEMM, "
+                       f"epilogue), extrapolated to M = {head['M']} and the 80-layer mixed mask; "
+                       f"{P} worker processes, one thread each"),
+            "host": {"cpu_count": cores, "affinity": aff, "workers": P}, "per_config": out["configs"],
+            "total_s": out["total_s"]}
+
+
+# ---------------------------------------------------------------------------
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the library has no multi-GPU path (the sharding plan is documented, not built)", file=sys.stderr)
+        print(f"bench.py measures one GPU (asked for --gpus {args.gpus}): the sharded path is a "
+              "design only, and every figure here is one GPU's", file=sys.stderr)
         sys.exit(2)
+    cpu = None
+    if not args.no_cpu_baseline and not args.only:
+        cpu = cpu_baseline(args.cpu_workers)      # before anything touches the GPU
     import torch
     import paper_2606_12487_amd as dptq
-    import workloads
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     dptq.lib()
-    cfg = workloads.CONFIGS["llama2_7b_qkv"]
-    M, K, N = cfg["M"], cfg["K"], cfg["N"]
     if args.only:
-        run_only(torch, dptq, cfg, args)
+        run_only(torch, dptq, args)
         return
 
-    wall, gpu_ms, seq, wall_graph = time_layer(torch, dptq, cfg, args)
-    ops_gemm = 2.0 * M * N * K
-    ops_step = ops_gemm * len(seq)
-    value = ops_step * args.steps / wall / 1e12
-    ms_step = wall * 1e3 / args.steps
-
-    per = time_kernels(torch, dptq, cfg, args, seq)
-    step_kernels = {"rotate_quant_fp6_a4": "rq_pow2_kernel<__half, 4, false, 12, false, true>",
-                    "gemm_fp6_a4": "qgemm_fp6<false, false>",
-                    "rotate_quant_a8": "rq_pow2_kernel<__half, 8, false, 12, false, false>",
-                    "gemm_a8": "qgemm_prefill_wide<8, false, true>"}
-    dominant = max(step_kernels, key=lambda k: per[k])
-    dom_ms = per[dominant]
-    fp6_ms = per["gemm_fp6_a4"]
-    k1_bytes = 2 * M * K + dptq.fp6_bytes(M, K) + 4 * M
-    rq6_ms = per["rotate_quant_fp6_a4"]
-    is_fp6 = dominant == "gemm_fp6_a4"
-    dom_peak = PEAK_FP6_TOPS if is_fp6 else PEAK_INT8_TOPS
-    dom_achieved = ops_gemm / (dom_ms * 1e-3) / 1e12
+    st, r = time_headline(torch, dptq, args)
+    value, ms, roof, kernels, extra = headline_record(st, r, args)
+    cfg5 = __import__("workloads").CONFIGS[HEADLINE]
     rec = {
-        "metric": METRIC, "value": round(value, 3), "unit": "TOPS", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int8",
+        "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int4 x int4 on fp6 MFMA, int8 x int4 on int8 MFMA, exact int32 sums",
         "data": "synthetic",
-        "config": {"workload": "llama2-7b fused qkv qlinear, rotate+quant+GEMM at A4 (fp6 matrix "
-                               "cores) then A8 (int8 matrix cores)",
-                   "M": M, "K": K, "N": N, "had_size": cfg["h"], "bits": list(seq),
-                   "parallelism": "none"},
-        "roofline": {"bound": "mfma", "kernel": step_kernels[dominant],
-                     "achieved": round(dom_achieved, 2), "peak": dom_peak,
-                     "unit": "TFLOP/s", "frac": round(dom_achieved / dom_peak, 4),
-                     "traffic": None if is_fp6 else measured_traffic()},
-        "roofline_fp6_gemm": {"bound": "mfma", "kernel": step_kernels["gemm_fp6_a4"],
-                              "achieved": round(ops_gemm / (fp6_ms * 1e-3) / 1e12, 2),
-                              "peak": PEAK_FP6_TOPS, "unit": "TFLOP/s",
-                              "frac": round(ops_gemm / (fp6_ms * 1e-3) / 1e12 / PEAK_FP6_TOPS, 4),
-                              "frac_of_int8_peak": round(ops_gemm / (fp6_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)},
-        "gpu_ms_per_step": round(gpu_ms / args.steps, 4),
-        "graph": {"value": round(ops_step * args.steps / wall_graph / 1e12, 3),
-                  "ms_per_step": round(wall_graph * 1e3 / args.steps, 4),
-                  "note": "the same steps replayed from captured HIP graphs"},
-        "kernels_ms": {k: round(v, 4) for k, v in per.items()},
-        "rotate_quant_fp6_a4": {"bound": "alu", "GB/s": round(k1_bytes / (rq6_ms * 1e-3) / 1e9, 1),
-                                "frac_of_hbm_peak": round(k1_bytes / (rq6_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "config": {"workload": "llama2-70b 80-layer linear stack (qkv 8192->10240, o 8192->8192, "
+                               "gate/up 8192->57344, down 28672->8192 at h=28x1024), M=4096 prefill, "
+                               "seeded mixed A4/A8 mask (4 of 80 layers at 8 bits)",
+                   "M": cfg5["M"], "layers": cfg5["L"], "mask": r["mask"], "parallelism": "none"},
+        "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4),
+        "gpu_ms_per_step": round(r["gpu_ms"], 3),
+        "roofline": roof,
+        "clocks": r["clocks"],
+        "headline": extra,
+        "kernels": kernels,
+        "setup_s": round(r["setup_s"], 1),
     }
-    # Decode GB/s (the metric's second half): config 3's down projection at
-    # M = 1, 4, 16, a few seconds.
-    rec["decode"] = time_decode(torch, dptq, args)
+    configs = {}
+    if not args.no_configs:
+        configs["llama2_70b_M8_decode"] = decode_70b(torch, st, r["bits"])
+    del st
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        progress("70B decode stack done")
+        configs["tiny"] = single_linear(torch, dptq, "tiny", 16)
+        configs["llama2_7b_qkv"] = single_linear(torch, dptq, "llama2_7b_qkv", 2048)
+        for M in (1, 4, 16, 2048):
+            configs[f"llama3_8b_down_M{M}"] = single_linear(torch, dptq, "llama3_8b_down", M)
+        progress("single linears done")
+        configs["llama2_7b_stack"] = stack_7b(torch, dptq)
+        progress("7B stack done")
+        rec["configs"] = configs
     if args.extended:
-        rec["decode_fused"] = time_decode_fused(torch, dptq)
-        rec["range_quantizer"] = time_range(torch, dptq, cfg)
-        rec["calibration"] = time_calibration(torch, dptq)
-        rec["kv4"] = time_kv(torch, dptq)
-        rec["stacks"] = {"llama2_7b_32_layers": time_stack(torch, dptq, "llama2_7b_stack", (2048, 8, 1)),
-                         "llama2_70b_80_layers": time_stack(torch, dptq, "llama2_70b_layer", (4096, 8, 1))}
-    if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(cfg, args.cpu_rows)
+        rec["extended"] = time_extended(torch, dptq)
+    if cpu is not None:
+        rec["cpu_baseline"] = cpu
     print(json.dumps(rec), flush=True)
 
 
