@@ -1,16 +1,21 @@
 """Turn rocprofv3 CSV output into the short text summaries kept under profiles/.
 
-    python -m paper_2606_12487_amd.rocprof_summary stats STATS_CSV [--title T] [--command C]
+    python -m paper_2606_12487_amd.rocprof_summary stats STATS_CSV [--top N] [--title T] [--command C]
     python -m paper_2606_12487_amd.rocprof_summary traffic FETCH_CSV WRITE_CSV \
         COPY_FETCH_CSV COPY_WRITE_CSV --kernel SUBSTR --source FILE \
-        --algorithmic-bytes B [--title T] [--command C]
+        --algorithmic-bytes B [--reduce mean|median] [--title T] [--command C]
+    python -m paper_2606_12487_amd.rocprof_summary trace TRACE_CSV --kernel SUBSTR \
+        --first N [--title T] [--command C]
 
 `stats` reads rocprofv3's kernel statistics (--kernel-trace --stats
 --output-format csv) and prints one row per kernel.  `traffic` reads two
 counter runs of a kernel (FETCH_SIZE, WRITE_SIZE: KiB per dispatch) and the
 same counters for a device copy of 256 MiB, scales the kernel's figures by
 known-bytes / counted-bytes of the copy, and prints HBM bytes per launch
-together with the kernel source digest they belong to.
+together with the kernel source digest they belong to.  `trace` reads the
+per-dispatch kernel trace and prints the mean duration of one kernel over its
+first N dispatches (a benchmark's headline launches, which come first) and
+over all of them.
 """
 
 import argparse
@@ -27,8 +32,10 @@ def _rows(path):
         return list(csv.DictReader(f))
 
 
-def stats(path, title, command):
+def stats(path, title, command, top=0):
     rows = _rows(path)
+    if top:
+        rows = sorted(rows, key=lambda r: -float(r.get("TotalDurationNs", 0)))[:top]
     out = [f"# {title}" if title else "# rocprofv3 kernel statistics"]
     if command:
         out.append(f"# command: {command}")
@@ -46,17 +53,38 @@ def stats(path, title, command):
     return "\n".join(out)
 
 
-def _counter(path, counter, kernel):
+def _counter(path, counter, kernel, reduce="median"):
     vals = [float(r["Counter_Value"]) for r in _rows(path)
             if r["Counter_Name"] == counter and kernel in r["Kernel_Name"]]
     if not vals:
         raise SystemExit(f"no {counter} rows for kernels matching {kernel!r} in {path}")
-    return statistics.median(vals), len(vals)
+    f = statistics.mean if reduce == "mean" else statistics.median
+    return f(vals), len(vals)
+
+
+def trace(path, kernel, first, title, command):
+    rows = [r for r in _rows(path) if kernel in r["Kernel_Name"]]
+    if not rows:
+        raise SystemExit(f"no dispatches of kernels matching {kernel!r} in {path}")
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    head = dur[:first]
+    out = [f"# {title}" if title else "# rocprofv3 kernel trace"]
+    if command:
+        out.append(f"# command: {command}")
+    out += [f"kernel: {kernel}",
+            f"dispatches_all: {len(dur)}",
+            f"average_us_all: {statistics.mean(dur):.2f}",
+            f"dispatches_first: {len(head)}",
+            f"average_us_first: {statistics.mean(head):.2f}",
+            f"min_us_first: {min(head):.2f}",
+            f"max_us_first: {max(head):.2f}"]
+    return "\n".join(out)
 
 
 def traffic(a, title, command):
-    fetch, nf = _counter(a.fetch_csv, "FETCH_SIZE", a.kernel)
-    write, nw = _counter(a.write_csv, "WRITE_SIZE", a.kernel)
+    fetch, nf = _counter(a.fetch_csv, "FETCH_SIZE", a.kernel, a.reduce)
+    write, nw = _counter(a.write_csv, "WRITE_SIZE", a.kernel, a.reduce)
     cfetch, _ = _counter(a.copy_fetch_csv, "FETCH_SIZE", a.copy_kernel)
     cwrite, _ = _counter(a.copy_write_csv, "WRITE_SIZE", a.copy_kernel)
     fscale = COPY_BYTES / (cfetch * 1024.0)
@@ -94,6 +122,7 @@ def main(argv=None):
     sub = p.add_subparsers(dest="cmd", required=True)
     s = sub.add_parser("stats")
     s.add_argument("csv")
+    s.add_argument("--top", type=int, default=0, help="only the N kernels with the most total time")
     s.add_argument("--title", default="")
     s.add_argument("--command", default="")
     t = sub.add_parser("traffic")
@@ -105,11 +134,20 @@ def main(argv=None):
     t.add_argument("--copy-kernel", default="")
     t.add_argument("--source", required=True)
     t.add_argument("--algorithmic-bytes", type=int, required=True)
+    t.add_argument("--reduce", choices=["median", "mean"], default="median")
     t.add_argument("--title", default="")
     t.add_argument("--command", default="")
+    r = sub.add_parser("trace")
+    r.add_argument("csv")
+    r.add_argument("--kernel", required=True)
+    r.add_argument("--first", type=int, required=True)
+    r.add_argument("--title", default="")
+    r.add_argument("--command", default="")
     a = p.parse_args(argv)
     if a.cmd == "stats":
-        print(stats(a.csv, a.title, a.command))
+        print(stats(a.csv, a.title, a.command, a.top))
+    elif a.cmd == "trace":
+        print(trace(a.csv, a.kernel, a.first, a.title, a.command))
     else:
         print(traffic(a, a.title, a.command))
 
