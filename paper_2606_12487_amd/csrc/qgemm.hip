@@ -197,6 +197,18 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
   return x * per + (x < rem ? x : rem) + idx;
 }
 
+// Tile (tm, tn) of logical tile `logical`: logical tiles run in groups of
+// kGroupM tile rows, m fastest within a group, so that the tiles an XCD works
+// on at one time form a compact block whose operands share its L2.
+__device__ __forceinline__ void grouped_tile(int logical, int tiles_m, int tiles_n, int& tm, int& tn) {
+  constexpr int kGroupM = 4;
+  const int per_group = kGroupM * tiles_n;
+  const int g = logical / per_group, t = logical - g * per_group;
+  const int gm = min(kGroupM, tiles_m - g * kGroupM);
+  tn = t / gm;
+  tm = g * kGroupM + (t - tn * gm);
+}
+
 template <int BITS, int BN, int BM, int WN, int WM>
 struct Cfg {
   static constexpr int kBits = BITS, kBN = BN, kBM = BM, kWN = WN, kWM = WM;
@@ -240,7 +252,8 @@ qgemm_prefill(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_s
   const int tiles_m = (M + kBM - 1) / kBM;
   const int tiles_n = (N + kBN - 1) / kBN;
   const int logical = xcd_remap(blockIdx.x, tiles_m * tiles_n);
-  const int tm = logical % tiles_m, tn = logical / tiles_m;
+  int tm, tn;
+  grouped_tile(logical, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * kBM, n0 = tn * kBN;
 
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -629,12 +642,13 @@ qgemm_prefill_wide(const uint8_t* __restrict__ a_codes, const float* __restrict_
   const int arow = BITS == 4 ? K / 2 : K;
   const int nst = K / C::kBK;
 
-  // Row origins of this workgroup's tile r.  Consecutive tiles of one XCD's
-  // workgroups are consecutive logical tiles (m fastest), so they share
-  // weight rows in that XCD's L2.
+  // Row origins of this workgroup's tile r.  The workgroups of one XCD take
+  // consecutive logical tiles, in groups of tile rows (grouped_tile), so the
+  // tiles in flight on an XCD share their operands in its L2.
   auto origin = [&](int r, int& m0, int& n0) __attribute__((always_inline)) {
     const int logical = xcd_remap((int)blockIdx.x + r * G, total);
-    const int tm = logical % tiles_m, tn = logical / tiles_m;
+    int tm, tn;
+    grouped_tile(logical, tiles_m, tiles_n, tm, tn);
     m0 = min(tm * C::kBM, M - C::kBM);
     n0 = min(tn * C::kBN, N - C::kBN);
   };

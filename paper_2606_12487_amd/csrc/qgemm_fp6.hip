@@ -245,12 +245,18 @@ __device__ __forceinline__ void qgemm_fp6_body(const uint8_t* __restrict__ a6,
   const int lane = threadIdx.x & 63;
 
   // Row origins of this workgroup's tile r (r clamped to its last tile).
-  // Consecutive tiles of one XCD's workgroups are consecutive logical tiles
-  // (m fastest), so they share weight rows in that XCD's L2.
+  // The workgroups of one XCD take consecutive logical tiles, and logical
+  // tiles run in groups of kGroupM tile rows, m fastest within a group: a
+  // round of 32 tiles on one XCD is a 4 (m) x 8 (n) block, whose operands
+  // (4 activation and 8 weight tiles) share that XCD's L2.
   auto origin = [&](int r, int& m0, int& n0) __attribute__((always_inline)) {
     r = min(r, ntile - 1);
     const int logical = f6_xcd_remap((int)blockIdx.x + r * G, total);
-    const int tm = logical % tiles_m, tn = logical / tiles_m;
+    constexpr int kGroupM = 4;
+    const int per_group = kGroupM * tiles_n;
+    const int g = logical / per_group, t = logical - g * per_group;
+    const int gm = min(kGroupM, tiles_m - g * kGroupM);
+    const int tn = t / gm, tm = g * kGroupM + (t - tn * gm);
     m0 = tm * C::kBM;
     n0 = tn * C::kBN;
     if constexpr (!CLAMP) {
