@@ -31,7 +31,7 @@ def test_bench_traffic_is_tied_to_the_kernel_source(tmp_path, monkeypatch):
     fake.write_text("source_sha256_16: 0000000000000000\nhbm_bytes_per_launch: 123\n")
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(fake))
     assert bench.measured_traffic() is None
-    fake.write_text(f"source_sha256_16: {bench.source_digest(bench.KERNEL_SOURCE)}\n"
+    fake.write_text(f"source_sha256_16: {bench.source_digest(bench.TRAFFIC_SOURCE)}\n"
                     "hbm_bytes_per_launch: 123\n")
     assert bench.measured_traffic() == 123
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.txt"))
