@@ -163,6 +163,17 @@ def graph_time(torch, fns, reps=5):
     return us
 
 
+def k1_essential_ops(h, fp6=False):
+    """Vector lane-operations per element rotate+quantize cannot avoid: log2 of
+    the power-of-two factor in butterflies, 27 additions of the 28-point stage
+    when h = 28 * 2^j (its pinned sequential order), 6 for widening, absmax,
+    the corrected quotient (multiply, two FMAs), rounding and packing, and 2
+    more for the FP6 operand (c / 2 and its fp16 conversion)."""
+    f28 = h % 28 == 0
+    p = h // 28 if f28 else h
+    return p.bit_length() - 1 + (27 if f28 else 0) + 6 + (2 if fp6 else 0)
+
+
 def k1_bytes(M, K, bits):
     """Algorithmic bytes of rotate+quantize: fp16 rows in, codes and scales out."""
     return 2 * M * K + M * K * bits // 8 + 4 * M
@@ -354,6 +365,8 @@ def headline_record(st, r, args):
             work = k1_bytes(M, K, b)
             ent["GB/s"] = round(work / (avg * 1e-6) / 1e9, 1)
             ent["frac_of_hbm_peak"] = round(ent["GB/s"] / PEAK_HBM_GBS, 4)
+            ops = k1_essential_ops(h, fp6="fp6" in kname) * M * K
+            ent["frac_of_alu_roof"] = round(ops / (avg * 1e-6) / PEAK_LANE_OPS, 4)
         kernels[f"{kname}/{ln}"] = ent
         f = fam.setdefault(kname, {"us": 0.0, "n": 0, "work": 0.0})
         f["us"] += sum(us)
@@ -424,6 +437,8 @@ def single_linear(torch, dptq, name, M, copies_bytes=300 << 20):
     def rec(k1_us, g_us, bits, path):
         r = {"rotate_quant_us": round(k1_us, 2), "gemm_us": round(g_us, 2),
              "rotate_quant_GB/s": round(k1_bytes(M, K, bits) / (k1_us * 1e-6) / 1e9, 1),
+             "rotate_quant_frac_of_alu_roof": round(
+                 k1_essential_ops(h, path == "fp6") * M * K / (k1_us * 1e-6) / PEAK_LANE_OPS, 4),
              "qlinear_TOPS": round(ops / ((k1_us + g_us) * 1e-6) / 1e12, 2),
              "gemm_TOPS": round(ops / (g_us * 1e-6) / 1e12, 2),
              "gemm_frac_of_int8_peak": round(ops / (g_us * 1e-6) / 1e12 / PEAK_INT8_TOPS, 4)}

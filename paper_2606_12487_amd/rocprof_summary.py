@@ -6,6 +6,8 @@
         --algorithmic-bytes B [--reduce mean|median] [--title T] [--command C]
     python -m paper_2606_12487_amd.rocprof_summary trace TRACE_CSV --kernel SUBSTR \
         --first N [--title T] [--command C]
+    python -m paper_2606_12487_amd.rocprof_summary counters CSV [CSV ...] --kernel SUBSTR \
+        --labels a,b,c [--skip N] [--title T] [--command C]
 
 `stats` reads rocprofv3's kernel statistics (--kernel-trace --stats
 --output-format csv) and prints one row per kernel.  `traffic` reads two
@@ -15,7 +17,9 @@ known-bytes / counted-bytes of the copy, and prints HBM bytes per launch
 together with the kernel source digest they belong to.  `trace` reads the
 per-dispatch kernel trace and prints the mean duration of one kernel over its
 first N dispatches (a benchmark's headline launches, which come first) and
-over all of them.
+over all of them.  `counters` reads counter passes of a run that launches a
+kernel at several shapes in a fixed cycle (after N other dispatches of it)
+and prints each counter's mean per dispatch for each shape of the cycle.
 """
 
 import argparse
@@ -117,6 +121,29 @@ def traffic(a, title, command):
     return "\n".join(out)
 
 
+def counters(paths, kernel, labels, skip, title, command):
+    per = {}   # counter -> dispatch id -> summed value
+    for path in paths:
+        for r in _rows(path):
+            if kernel in r["Kernel_Name"]:
+                d = per.setdefault(r["Counter_Name"], {})
+                i = int(r["Dispatch_Id"])
+                d[i] = d.get(i, 0.0) + float(r["Counter_Value"])
+    out = [f"# {title}" if title else "# rocprofv3 counters per dispatch"]
+    if command:
+        for c in command.split(" ;; "):
+            out.append(f"# command: {c}")
+    out.append("counter | " + " | ".join(labels))
+    for name in sorted(per):
+        ids = sorted(per[name])[skip:]
+        cols = [[] for _ in labels]
+        for k, i in enumerate(ids):
+            cols[k % len(labels)].append(per[name][i])
+        out.append(name + " | " + " | ".join(
+            f"{statistics.mean(c):.0f}" if c else "-" for c in cols))
+    return "\n".join(out)
+
+
 def main(argv=None):
     p = argparse.ArgumentParser()
     sub = p.add_subparsers(dest="cmd", required=True)
@@ -143,7 +170,17 @@ def main(argv=None):
     r.add_argument("--first", type=int, required=True)
     r.add_argument("--title", default="")
     r.add_argument("--command", default="")
+    c = sub.add_parser("counters")
+    c.add_argument("csv", nargs="+")
+    c.add_argument("--kernel", required=True)
+    c.add_argument("--labels", required=True)
+    c.add_argument("--skip", type=int, default=0)
+    c.add_argument("--title", default="")
+    c.add_argument("--command", default="")
     a = p.parse_args(argv)
+    if a.cmd == "counters":
+        print(counters(a.csv, a.kernel, a.labels.split(","), a.skip, a.title, a.command))
+        return
     if a.cmd == "stats":
         print(stats(a.csv, a.title, a.command, a.top))
     elif a.cmd == "trace":
