@@ -206,6 +206,8 @@ RQ6_CASES = [
     # more than 64 rows: the segmented kernel (28 * 2^j, 2^j above 4096, a
     # partial last segment, ragged 32-row blocks)
     (70, 8192, 8192), (100, 14336, 28 * 512), (97, 12544, 28 * 64),
+    # rows that leave room for one per compute unit (four thread groups)
+    (66, 28672, 28 * 1024), (65, 24576, 8192),
 ]
 
 

@@ -78,7 +78,8 @@ ROT_CASES = [
     (3, 4096, 512), (2, 16384, 16384), (5, 12288, 4096), (4, 4160, 64),
     (3, 4224, 128), (2, 4104, 8), (3, 4120, 8),
     # more than 64 rows so long that one compute unit holds one of them
-    # (1024 threads per row, as for decode)
+    # (1024 threads per row in four groups; 7 and 6 segments, so the groups
+    # take unequal shares)
     (70, 28672, 28 * 1024), (66, 24576, 8192),
     # more than 64 rows of up to 16384 with h = 28 * 2^j or 2^j above 4096:
     # the segmented kernel (one partial segment, block-diagonal sizes, the
