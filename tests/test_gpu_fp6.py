@@ -146,6 +146,32 @@ def test_fp6_end_to_end_tiny(dev):
     assert np.array_equal(y.view(np.uint16), ref.view(np.uint16))
 
 
+PARTIAL_ROUND_CASES = [
+    # (M, N, K): tile counts (256 x 192 tiles) that leave the last round over
+    # the compute units partly empty or run below one round: 128, 150 and 176
+    # tiles, and one whole round plus 64 or 96 tiles
+    (512, 12288, 4096), (1280, 5760, 4096), (2048, 4096, 4096), (2048, 7680, 4096),
+    (256, 67584, 4096),
+]
+
+
+@pytest.mark.parametrize("M,N,K", PARTIAL_ROUND_CASES)
+def test_fp6_partial_round_matches_oracle(dev, M, N, K):
+    from paritylib import assert_acc, oracle_y, safe_w_scales
+    rng = np.random.default_rng([M, N, K])
+    a = workloads.random_weight_bytes(rng, M, K)
+    w = workloads.random_weight_bytes(rng, N, K)
+    a_s = workloads.random_scales(rng, M, 1e-3, 1.0)
+    w_s = safe_w_scales(rng, N, K, a_s, 4)
+    a6, w6 = _fp6_operands(dev, a, w)
+    acc_ref = qlinear_acc_ref(a, 4, w)
+    assert_acc(_h(dptq.qlinear_fp6_acc(a6, w6, M, K, N)), acc_ref, f"{M}x{N}x{K} acc")
+    y = _h(dptq.qlinear_fp6(a6, _d(a_s, dev), w6, _d(w_s, dev), M, K, N))
+    y_ref = oracle_y(acc_ref, a_s, w_s)
+    bad = np.nonzero(y.view(np.uint16) != y_ref.view(np.uint16))
+    assert bad[0].size == 0, f"{bad[0].size} outputs differ, first at {bad[0][0]},{bad[1][0]}"
+
+
 FULL_SHAPES = [
     # (name, M, K, N): LLaMA-2-7B fused QKV, LLaMA-3-8B down_proj prefill,
     # LLaMA-2-70B qkv and down_proj prefill
