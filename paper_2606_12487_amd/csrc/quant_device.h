@@ -40,6 +40,97 @@ struct Paley28 {
 };
 constexpr Paley28 kH28{};
 
+// The dense 28-point stage sums column b as acc = +-z[0], then acc +-= z[a]
+// for a = 1 .. 27 in order, signs from H28[a][b].  Two columns whose signs
+// agree on rows 0 .. a, up to one common sign flip, hold partial sums that
+// are equal or exact negatives of each other (fp32 negation is exact and
+// round-to-nearest-even is symmetric), so one value serves both; 634 adds
+// instead of 756 give the 28 outputs bit for bit.  H28Trie<B0, NB> is that
+// sharing plan for columns B0 .. B0 + NB - 1: at depth a, node n continues
+// node par[a][n] of depth a - 1, negated when psg < 0, with +-z[a] by zsg;
+// the node of the first (lowest) column in a class holds that column's own
+// sum, so at depth 27, where every column has a node of its own, fin[b] is
+// the node holding output B0 + b.
+template <int B0, int NB>
+struct H28Trie {
+  int cnt[28];
+  signed char par[28][28], psg[28][28], zsg[28][28], fin[28];
+  constexpr H28Trie() : cnt{}, par{}, psg{}, zsg{}, fin{} {
+    int rep[28][NB] = {}, node_of[28][NB] = {}, sig[28][NB] = {};
+    for (int a = 0; a < 28; ++a) {
+      int reps = 0;
+      for (int i = 0; i < NB; ++i) {
+        const int b = B0 + i;
+        rep[a][i] = -1;
+        for (int k = 0; k < i && rep[a][i] < 0; ++k) {
+          const int c = B0 + k;
+          if (rep[a][k] != k) continue;            // compare with class leaders only
+          const int f = kH28.e[0][b] * kH28.e[0][c];
+          bool same = true;
+          for (int r = 0; r <= a; ++r) same = same && kH28.e[r][b] == f * kH28.e[r][c];
+          if (same) {
+            rep[a][i] = k;
+            sig[a][i] = f;
+            node_of[a][i] = node_of[a][k];
+          }
+        }
+        if (rep[a][i] < 0) {
+          rep[a][i] = i;
+          sig[a][i] = 1;
+          node_of[a][i] = reps++;
+        }
+      }
+      cnt[a] = reps;
+      if (a > 0) {
+        for (int i = 0; i < NB; ++i) {
+          if (rep[a][i] != i) continue;
+          const int n = node_of[a][i];
+          par[a][n] = (signed char)node_of[a - 1][i];
+          psg[a][n] = (signed char)sig[a - 1][i];
+          zsg[a][n] = kH28.e[a][B0 + i];
+        }
+      } else {
+        zsg[0][0] = kH28.e[0][B0];
+      }
+    }
+    for (int i = 0; i < NB; ++i) fin[i] = (signed char)(sig[27][i] == 1 ? node_of[27][i] : -1);
+  }
+};
+
+// Outputs B0 .. B0 + NB - 1 of one column of the 28-point stage from its 28
+// inputs z: out(b, value) for each, b counted from 0.
+template <int B0, int NB>
+constexpr bool h28_trie_complete(const H28Trie<B0, NB>& t) {
+  if (t.cnt[27] != NB) return false;
+  for (int b = 0; b < NB; ++b)
+    if (t.fin[b] < 0) return false;
+  return true;
+}
+
+template <int B0, int NB, typename Out>
+__host__ __device__ __forceinline__ void h28_column(const float* z, Out out) {
+  constexpr H28Trie<B0, NB> t{};
+  static_assert(h28_trie_complete(t), "every column ends on a node of its own, unnegated");
+  float nd[NB];
+  nd[0] = t.zsg[0][0] > 0 ? z[0] : -z[0];
+#pragma unroll
+  for (int a = 1; a < 28; ++a) {
+    float nn[NB];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      if (n < t.cnt[a]) {
+        const float pv = t.psg[a][n] > 0 ? nd[t.par[a][n]] : -nd[t.par[a][n]];
+        nn[n] = t.zsg[a][n] > 0 ? pv + z[a] : pv - z[a];
+      }
+    }
+#pragma unroll
+    for (int n = 0; n < NB; ++n)
+      if (n < t.cnt[a]) nd[n] = nn[n];
+  }
+#pragma unroll
+  for (int b = 0; b < NB; ++b) out(b, nd[t.fin[b]]);
+}
+
 // Code bits of y / s rounded to nearest, ties to even: t + 1.5 * 2^23 leaves
 // round(t) in the low mantissa bits (two's complement), from which nibbles
 // and bytes are packed.  |code| <= qmax holds without a clamp: |t| <=
@@ -297,14 +388,10 @@ __device__ __forceinline__ void rotate_row_segments(const __half* __restrict__ x
           float z[28];
 #pragma unroll
           for (int a = 0; a < 28; ++a) z[a] = rh[seg_index(base + a * p)];
-#pragma unroll
-          for (int bb = 0; bb < 28; ++bb) {
-            float acc = kH28.e[0][bb] > 0 ? z[0] : -z[0];
-#pragma unroll
-            for (int a = 1; a < 28; ++a) acc = kH28.e[a][bb] > 0 ? acc + z[a] : acc - z[a];
+          h28_column<0, 28>(z, [&](int bb, float acc) __attribute__((always_inline)) {
             rh[seg_index(base + bb * p)] = acc;
             row_max1<RANGE>(acc, ma, mb);
-          }
+          });
         }
       }
     }

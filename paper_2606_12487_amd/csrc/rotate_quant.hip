@@ -107,17 +107,13 @@ __device__ __forceinline__ float pass_bits(float* lds, int K, int s, bool last, 
 
 // Dense 28-point stage: y[b*p + c] = sum over a = 0..27 (in order) of
 // H28[a][b] * z[a*p + c], per block and fast index c.  Outputs B0 .. B0+NB-1
-// of one column from its 28 inputs z.
+// of one column from its 28 inputs z (shared partial sums, h28_column).
 template <int NB, int B0>
 __device__ __forceinline__ float dense28(float* lds, int base, int p, const float* z, float tmax) {
-#pragma unroll
-  for (int b = B0; b < B0 + NB; ++b) {
-    float acc = kH28.e[0][b] > 0 ? z[0] : -z[0];
-#pragma unroll
-    for (int a = 1; a < 28; ++a) acc = kH28.e[a][b] > 0 ? acc + z[a] : acc - z[a];
-    lds[lidx(base + b * p)] = acc;
+  h28_column<B0, NB>(z, [&](int b, float acc) __attribute__((always_inline)) {
+    lds[lidx(base + (B0 + b) * p)] = acc;
     tmax = fmaxf(tmax, fabsf(acc));
-  }
+  });
   return tmax;
 }
 
