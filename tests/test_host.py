@@ -41,3 +41,22 @@ def test_bench_traffic_is_tied_to_the_kernel_source(tmp_path, monkeypatch):
 def test_entry_module_has_build_and_smoke():
     import __graft_entry__ as g
     assert callable(g.build) and callable(g.smoke)
+
+
+def test_h28_shared_partial_sums_match_in_order_sums(tmp_path):
+    # The kernels' 28-point stage shares partial sums between columns; a host
+    # build of that routine must give the in-order sums bit for bit.
+    import shutil
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    exe = tmp_path / "h28_check"
+    src = os.path.join(ROOT, "tests", "h28_prefix_check.cpp")
+    csrc = os.path.join(ROOT, "paper_2606_12487_amd", "csrc")
+    r = subprocess.run([hipcc, "-O2", "-std=c++20", "-ffp-contract=off", f"-I{csrc}", "-x", "hip",
+                        "--offload-arch=gfx950", src, "-o", str(exe)],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert run.returncode == 0, run.stdout + run.stderr
+    assert "28 columns 0," in run.stdout
