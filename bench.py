@@ -365,8 +365,8 @@ def headline_record(st, r, args):
             work = k1_bytes(M, K, b)
             ent["GB/s"] = round(work / (avg * 1e-6) / 1e9, 1)
             ent["frac_of_hbm_peak"] = round(ent["GB/s"] / PEAK_HBM_GBS, 4)
-            ops = k1_essential_ops(h, fp6="fp6" in kname) * M * K
-            ent["frac_of_alu_roof"] = round(ops / (avg * 1e-6) / PEAK_LANE_OPS, 4)
+            lane_ops = k1_essential_ops(h, fp6="fp6" in kname) * M * K
+            ent["frac_of_alu_roof"] = round(lane_ops / (avg * 1e-6) / PEAK_LANE_OPS, 4)
         kernels[f"{kname}/{ln}"] = ent
         f = fam.setdefault(kname, {"us": 0.0, "n": 0, "work": 0.0})
         f["us"] += sum(us)

@@ -813,9 +813,11 @@ hipError_t dispatch_seg(HadSplit hs, const __half* x, int64_t M, int K, uint8_t*
 // goes to the segmented kernel while its staging leaves room for two rows per
 // compute unit (K <= 16384); longer rows keep the 1024-thread general kernel,
 // which was 1.5x faster at K = 28672 (28 x 1024) than one 256-thread row per
-// compute unit.
-bool use_seg(int64_t M, int K, HadSplit hs) {
-  return kSegRows > 0 && M > kSegRows && K % 128 == 0 && (hs.f == 28 || hs.j > 12) &&
+// compute unit.  FP6-layout output at power-of-two sizes stays on the general
+// kernel too, which was as fast or faster there (38.0 vs 38.5 us at
+// 4096 x 8192, h = 8192).
+bool use_seg(int64_t M, int K, HadSplit hs, bool fp6) {
+  return kSegRows > 0 && M > kSegRows && K % 128 == 0 && (hs.f == 28 || (hs.j > 12 && !fp6)) &&
          seg_lds_bytes(K) <= kOneRowLds;
 }
 
@@ -827,7 +829,7 @@ hipError_t launch_rq(const Tin* x, int64_t M, int K, HadSplit hs, uint8_t* codes
                      const uint8_t* signs = nullptr) {
   if (M == 0) return hipSuccess;
   if constexpr (!WEIGHT && !STATS && sizeof(Tin) == 2) {
-    if (signs == nullptr && use_seg(M, K, hs))
+    if (signs == nullptr && use_seg(M, K, hs, FP6))
       return dispatch_seg<BITS, FP6>(hs, reinterpret_cast<const __half*>(x), M, K, codes, scales,
                                      stream);
   }
