@@ -84,68 +84,106 @@ __device__ __forceinline__ float absmax8(const float* v, float m) {
 }
 
 
-// One pass over index bits [s, s+G): each work item gathers the 2^G elements
-// that differ only in those bits, applies the butterflies, and writes back.
-template <int G, int T>
-__device__ __forceinline__ float pass_bits(float* lds, int K, int s, bool last, float tmax) {
+// lidx(b | o) = lidx(b) + lidx(o) whenever b and o share no set bit (the
+// shift that forms the padding distributes over a disjoint OR), so an element
+// at a constant bit pattern o from a base b is a constant offset from lidx(b)
+// in LDS, which the LDS instructions take as an immediate.
+constexpr int lidx_c(int i) { return i + ((i >> 8) << 3); }
+
+// One pass over index bits [S, S+G): each work item gathers the 2^G elements
+// that differ only in those bits (base with those bits clear, plus k << S),
+// applies the butterflies, and writes back.
+template <int G, int S, int T>
+__device__ __forceinline__ float pass_bits(float* lds, int K, bool last, float tmax) {
   const int groups = K >> G;
-  const int low_mask = (1 << s) - 1;
+  constexpr int low_mask = (1 << S) - 1;
   for (int g = threadIdx.x; g < groups; g += T) {
-    const int base = (g & low_mask) | ((g >> s) << (s + G));
+    const int base = (g & low_mask) | ((g >> S) << (S + G));
+    const float* src = lds + lidx(base);
     float v[1 << G];
 #pragma unroll
-    for (int k = 0; k < (1 << G); ++k) v[k] = lds[lidx(base + (k << s))];
+    for (int k = 0; k < (1 << G); ++k) v[k] = src[lidx_c(k << S)];
     butterflies<G>(v, 0, G);
+    float* dst = lds + lidx(base);
 #pragma unroll
     for (int k = 0; k < (1 << G); ++k) {
-      lds[lidx(base + (k << s))] = v[k];
+      dst[lidx_c(k << S)] = v[k];
       if (last) tmax = fmaxf(tmax, fabsf(v[k]));
     }
   }
   return tmax;
 }
 
+// Element a (slow index) of a 28-point column at base: lidx(base + a p).
+// With p = 2^J >= 256 the padding splits (base's fast part lies below bit J,
+// and a p adds whole multiples of 256), so it is lidx(base) plus the constant
+// a (p + p / 32); the column then reads from two bases, 14 rows apart, so that
+// every offset fits the LDS instructions' immediate.  Below 256 it is
+// computed per element.
+template <int J>
+struct Col28 {
+  static constexpr int kP = 1 << J;
+  static constexpr bool kSplit = J >= 8;
+  static constexpr int kStep = kP + kP / 32;
+  float* b0;
+  float* b1;
+  int base;
+  __device__ __forceinline__ Col28(float* lds, int base_) : base(base_) {
+    if constexpr (kSplit) {
+      b0 = lds + lidx(base_);
+      b1 = b0 + 14 * kStep;
+    } else {
+      b0 = lds;
+      b1 = lds;
+    }
+  }
+  __device__ __forceinline__ float& at(int a) const {
+    if constexpr (kSplit) return a < 14 ? b0[a * kStep] : b1[(a - 14) * kStep];
+    else return b0[lidx(base + a * kP)];
+  }
+};
+
 // Dense 28-point stage: y[b*p + c] = sum over a = 0..27 (in order) of
 // H28[a][b] * z[a*p + c], per block and fast index c.  Outputs B0 .. B0+NB-1
 // of one column from its 28 inputs z (shared partial sums, h28_column).
-template <int NB, int B0>
-__device__ __forceinline__ float dense28(float* lds, int base, int p, const float* z, float tmax) {
+template <int NB, int B0, int J>
+__device__ __forceinline__ float dense28(const Col28<J>& col, const float* z, float tmax) {
   h28_column<B0, NB>(z, [&](int b, float acc) __attribute__((always_inline)) {
-    lds[lidx(base + (B0 + b) * p)] = acc;
+    col.at(B0 + b) = acc;
     tmax = fmaxf(tmax, fabsf(acc));
   });
   return tmax;
 }
 
-template <int T>
-__device__ __forceinline__ float pass_28(float* lds, int K, int j, float tmax) {
-  const int p = 1 << j;
+template <int T, int J>
+__device__ __forceinline__ float pass_28(float* lds, int K, float tmax) {
+  constexpr int p = 1 << J;
   const int cols = K / 28;
   if (2 * cols <= T && cols % 64 == 0) {
     // Two threads per column (wavefront-uniform halves), each writing 14 of
     // its outputs; every input is read before any output is written.
     const int t = threadIdx.x;
     const bool active = t < 2 * cols;
-    const int col = t % cols, half = t / cols;
-    const int base = (col >> j) * 28 * p + (col & (p - 1));
+    const int c = t % cols, half = t / cols;
+    const Col28<J> col(lds, (c >> J) * 28 * p + (c & (p - 1)));
     float z[28];
     if (active) {
 #pragma unroll
-      for (int a = 0; a < 28; ++a) z[a] = lds[lidx(base + a * p)];
+      for (int a = 0; a < 28; ++a) z[a] = col.at(a);
     }
     __syncthreads();
     if (active) {
-      if (half == 0) tmax = dense28<14, 0>(lds, base, p, z, tmax);
-      else tmax = dense28<14, 14>(lds, base, p, z, tmax);
+      if (half == 0) tmax = dense28<14, 0, J>(col, z, tmax);
+      else tmax = dense28<14, 14, J>(col, z, tmax);
     }
     return tmax;
   }
-  for (int col = threadIdx.x; col < cols; col += T) {
-    const int base = (col >> j) * 28 * p + (col & (p - 1));
+  for (int c = threadIdx.x; c < cols; c += T) {
+    const Col28<J> col(lds, (c >> J) * 28 * p + (c & (p - 1)));
     float z[28];
 #pragma unroll
-    for (int a = 0; a < 28; ++a) z[a] = lds[lidx(base + a * p)];
-    tmax = dense28<28, 0>(lds, base, p, z, tmax);
+    for (int a = 0; a < 28; ++a) z[a] = col.at(a);
+    tmax = dense28<28, 0, J>(col, z, tmax);
   }
   return tmax;
 }
@@ -318,19 +356,19 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
   __syncthreads();
 
   if constexpr (P::np > 0) {
-    tmax = pass_bits<P::width(0), T>(lds, K, P::start(0), P::np == 1 && F == 1, tmax);
+    tmax = pass_bits<P::width(0), P::start(0), T>(lds, K, P::np == 1 && F == 1, tmax);
     __syncthreads();
   }
   if constexpr (P::np > 1) {
-    tmax = pass_bits<P::width(1), T>(lds, K, P::start(1), P::np == 2 && F == 1, tmax);
+    tmax = pass_bits<P::width(1), P::start(1), T>(lds, K, P::np == 2 && F == 1, tmax);
     __syncthreads();
   }
   if constexpr (P::np > 2) {
-    tmax = pass_bits<P::width(2), T>(lds, K, P::start(2), F == 1, tmax);
+    tmax = pass_bits<P::width(2), P::start(2), T>(lds, K, F == 1, tmax);
     __syncthreads();
   }
   if constexpr (F == 28) {
-    tmax = pass_28<T>(lds, K, J, tmax);
+    tmax = pass_28<T, J>(lds, K, tmax);
     __syncthreads();
   }
 
