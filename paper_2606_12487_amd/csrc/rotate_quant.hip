@@ -701,37 +701,25 @@ rq_pow2_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __restric
 }
 
 // ---------------------------------------------------------------------------
-// Many rows (prefill) of h = 2^j above 4096 or h = 28 * 2^j: the segmented
+// Many rows (prefill) of h = 2^j, j >= 14, at 4 or 8 bits: the segmented
 // rotation of quant_device.h (three register phases over 4096-element
-// segments with compile-time LDS offsets, one LDS pass per index bit above
-// 11 pairing whole segments, then the 28-point columns, all in the pinned
-// order), one row per 256-thread workgroup, then the quantizer and outputs
-// of rq_pow2_kernel on the phase-1 layout.  K % 128 == 0.
+// segments with compile-time LDS offsets, one LDS pass per index bit above 11
+// pairing whole segments, in the pinned order), one row per 256-thread
+// workgroup, then the quantizer and the nibble or byte output of
+// rq_pow2_kernel on the phase-1 layout.  K % 128 == 0.
 // ---------------------------------------------------------------------------
-template <int BITS, int JP, bool F28, bool FP6>
+template <int BITS>
 __global__ void __launch_bounds__(kThreads)
 rq_seg_kernel(const __half* __restrict__ x, int M, int K, int J, uint8_t* __restrict__ codes,
               float* __restrict__ scales) {
-  static_assert(!FP6 || BITS == 4, "FP6 output holds 4-bit codes");
   extern __shared__ float lds[];
   __shared__ float red[kThreads / 64];
-  const int mblk = (M + 31) >> 5;
-  const int row = FP6 ? fp6_row(blockIdx.x, mblk * 32) : (int)blockIdx.x;
+  const int row = (int)blockIdx.x;
   const int t = threadIdx.x;
-  if constexpr (FP6) {
-    if (row >= M) {   // padding row of the last block: zero codes
-      for (int q = t; q < K / 32; q += kThreads) {
-        uint8_t* d = codes + fp6_slot(row, 32 * q, mblk);
-#pragma unroll
-        for (int c = 0; c < 3; ++c) *reinterpret_cast<uint2*>(d + 512 * c) = make_uint2(0, 0);
-      }
-      return;
-    }
-  }
   const uint4 none[2] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
   float ma = 0.0f, mb = 0.0f;
-  rotate_row_segments<JP, F28, false, 1>(x + (size_t)row * K, K, J, true, t,
-                                         RowSplit{0, 1, t, kThreads}, false, none, lds, ma, mb);
+  rotate_row_segments<12, false, false, 1>(x + (size_t)row * K, K, J, true, t,
+                                           RowSplit{0, 1, t, kThreads}, false, none, lds, ma, mb);
   ma = wave_max_nonneg(ma);
   if ((t & 63) == 0) red[t >> 6] = ma;
   __syncthreads();
@@ -759,17 +747,7 @@ rq_seg_kernel(const __half* __restrict__ x, int M, int K, int J, uint8_t* __rest
       bt[4 * q + 2] = round_bits(w4.z, sc, rc);
       bt[4 * q + 3] = round_bits(w4.w, sc, rc);
     }
-    if constexpr (FP6) {
-      const f6_v6i f = fp6_fields<16>(bt);
-      uint8_t* d = codes + fp6_slot(row, e, mblk);
-      if ((e & 16) == 0) {
-        *reinterpret_cast<uint2*>(d) = make_uint2((uint32_t)f[0], (uint32_t)f[1]);
-        *reinterpret_cast<uint32_t*>(d + 512) = (uint32_t)f[2];
-      } else {
-        *reinterpret_cast<uint32_t*>(d + 516) = (uint32_t)f[0];
-        *reinterpret_cast<uint2*>(d + 1024) = make_uint2((uint32_t)f[1], (uint32_t)f[2]);
-      }
-    } else if (BITS == 4) {
+    if constexpr (BITS == 4) {
       *reinterpret_cast<uint2*>(codes + (size_t)row * (K / 2) + e / 2) =
           make_uint2(pack_nibbles(bt), pack_nibbles(bt + 8));
     } else {
@@ -815,10 +793,10 @@ hipError_t dispatch_pow2(int j, const Tin* x, int64_t M, int K, const uint8_t* s
 
 size_t seg_lds_bytes(int K) { return (size_t)((K + kSeg - 1) / kSeg) * kSegFloats * sizeof(float); }
 
-template <int BITS, int JP, bool F28, bool FP6>
-hipError_t launch_seg_t(const __half* x, int64_t M, int K, int J, uint8_t* codes, float* scales,
-                        hipStream_t stream) {
-  auto kern = rq_seg_kernel<BITS, JP, F28, FP6>;
+template <int BITS>
+hipError_t launch_seg(const __half* x, int64_t M, int K, int J, uint8_t* codes, float* scales,
+                      hipStream_t stream) {
+  auto kern = rq_seg_kernel<BITS>;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -827,35 +805,19 @@ hipError_t launch_seg_t(const __half* x, int64_t M, int K, int J, uint8_t* codes
     (void)hipGetLastError();
     attr_set = true;
   }
-  const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), seg_lds_bytes(K), stream, x, (int)M,
+  hipLaunchKernelGGL(kern, dim3((unsigned)M), dim3(kThreads), seg_lds_bytes(K), stream, x, (int)M,
                      K, J, codes, scales);
   return hipGetLastError();
 }
 
-// h = 28 * 2^j (j <= 10) and 2^j above 4096 (JP = 12).
-template <int BITS, bool FP6, int JP = 0>
-hipError_t dispatch_seg(HadSplit hs, const __half* x, int64_t M, int K, uint8_t* codes, float* scales,
-                        hipStream_t stream) {
-  if constexpr (JP == 12) {
-    return launch_seg_t<BITS, 12, false, FP6>(x, M, K, hs.j, codes, scales, stream);
-  } else {
-    if (hs.f == 28 && hs.j == JP) {
-      if constexpr (JP <= 10) return launch_seg_t<BITS, JP, true, FP6>(x, M, K, hs.j, codes, scales, stream);
-    }
-    return dispatch_seg<BITS, FP6, JP + 1>(hs, x, M, K, codes, scales, stream);
-  }
-}
-
-// Plain fp16 rotation of many rows with a large or 28 * 2^j Hadamard size
-// goes to the segmented kernel while its staging leaves room for two rows per
-// compute unit (K <= 16384); longer rows keep the 1024-thread general kernel,
-// which was 1.5x faster at K = 28672 (28 x 1024) than one 256-thread row per
-// compute unit.  FP6-layout output at power-of-two sizes stays on the general
-// kernel too, which was as fast or faster there (38.0 vs 38.5 us at
-// 4096 x 8192, h = 8192).
+// Plain fp16 rotation of many rows at h = 2^j, j >= 14, with nibble or byte
+// output goes to the segmented kernel while its staging leaves room for two
+// rows per compute unit (K <= 16384): 85.5 / 86.6 us against 90.0 / 94.1 us
+// for the general kernel at 4096 x 16384 (A4 / A8).  Everywhere else the
+// general kernel, with its constant-offset LDS addressing, was as fast or
+// faster: at 28 * 2^j by 4-12%, at 8192 by 1-4%.
 bool use_seg(int64_t M, int K, HadSplit hs, bool fp6) {
-  return kSegRows > 0 && M > kSegRows && K % 128 == 0 && (hs.f == 28 || (hs.j > 12 && !fp6)) &&
+  return kSegRows > 0 && M > kSegRows && K % 128 == 0 && hs.f == 1 && hs.j >= 14 && !fp6 &&
          seg_lds_bytes(K) <= kOneRowLds;
 }
 
@@ -867,9 +829,11 @@ hipError_t launch_rq(const Tin* x, int64_t M, int K, HadSplit hs, uint8_t* codes
                      const uint8_t* signs = nullptr) {
   if (M == 0) return hipSuccess;
   if constexpr (!WEIGHT && !STATS && sizeof(Tin) == 2) {
-    if (signs == nullptr && use_seg(M, K, hs, FP6))
-      return dispatch_seg<BITS, FP6>(hs, reinterpret_cast<const __half*>(x), M, K, codes, scales,
-                                     stream);
+    if constexpr (!FP6) {
+      if (signs == nullptr && use_seg(M, K, hs, FP6))
+        return launch_seg<BITS>(reinterpret_cast<const __half*>(x), M, K, hs.j, codes, scales,
+                                stream);
+    }
   }
   if (hs.f == 28)
     return dispatch_j<Tin, BITS, WEIGHT, 28, STATS, FP6>(hs.j, x, M, K, signs, codes, scales, st,

@@ -229,8 +229,8 @@ RQ6_CASES = [
     (1, 128, 128), (5, 256, 16), (33, 1024, 1024), (64, 4096, 4096), (70, 4096, 256),
     (3, 14336, 28 * 512), (40, 3584, 28 * 128), (2, 8192, 8192), (31, 11008 - 11008 % 128, 128),
     (130, 4096, 4096),
-    # more than 64 rows: the segmented kernel (28 * 2^j, 2^j above 4096, a
-    # partial last segment, ragged 32-row blocks)
+    # more than 64 rows (28 * 2^j, 2^j above 4096, a partial last 4096-element
+    # segment, ragged 32-row blocks)
     (70, 8192, 8192), (100, 14336, 28 * 512), (97, 12544, 28 * 64),
     # rows that leave room for one per compute unit (four thread groups)
     (66, 28672, 28 * 1024), (65, 24576, 8192),

@@ -81,9 +81,9 @@ ROT_CASES = [
     # (1024 threads per row in four groups; 7 and 6 segments, so the groups
     # take unequal shares)
     (70, 28672, 28 * 1024), (66, 24576, 8192),
-    # more than 64 rows of up to 16384 with h = 28 * 2^j or 2^j above 4096:
-    # the segmented kernel (one partial segment, block-diagonal sizes, the
-    # largest row it takes)
+    # more than 64 rows of up to 16384 with h = 28 * 2^j or 2^j above 4096
+    # (a partial last 4096-element segment, block-diagonal sizes); at
+    # h = 16384 the segmented kernel
     (65, 8192, 8192), (100, 14336, 28 * 512), (72, 16384, 16384), (80, 7168, 28 * 256),
     (66, 3584, 28 * 128), (67, 16384, 8192), (129, 12544, 28 * 64),
 ]
