@@ -33,8 +33,18 @@ constexpr int kThreads = 256;
 // 28 * 2^j Hadamard sizes (0: never).
 constexpr int64_t kSegRows = 64;
 
-// LDS index of row element i: 8 floats of padding after every 256.
-__device__ __forceinline__ int lidx(int i) { return i + ((i >> 8) << 3); }
+// LDS index of row element i in the general kernel: PD = 0 pads 8 floats
+// after every 256, PD = 1 pads 4 after every 32 (more room, fewer bank
+// conflicts for the 28 * 2^j passes at j = 9 and 10, where rows are at most
+// 28672 long).
+template <int PD>
+__host__ __device__ constexpr int lidx(int i) {
+  return PD == 0 ? i + ((i >> 8) << 3) : i + ((i >> 5) << 2);
+}
+template <int F, int J>
+constexpr int pad_of() {
+  return (F == 28 && (J == 9 || J == 10)) ? 1 : 0;
+}
 
 // Radix-2 butterflies on v[0..2^G) over local bits lo .. lo+nb-1, low bit first.
 template <int G>
@@ -88,26 +98,25 @@ __device__ __forceinline__ float absmax8(const float* v, float m) {
 // shift that forms the padding distributes over a disjoint OR), so an element
 // at a constant bit pattern o from a base b is a constant offset from lidx(b)
 // in LDS, which the LDS instructions take as an immediate.
-constexpr int lidx_c(int i) { return i + ((i >> 8) << 3); }
 
 // One pass over index bits [S, S+G): each work item gathers the 2^G elements
 // that differ only in those bits (base with those bits clear, plus k << S),
 // applies the butterflies, and writes back.
-template <int G, int S, int T>
+template <int G, int S, int T, int PD>
 __device__ __forceinline__ float pass_bits(float* lds, int K, bool last, float tmax) {
   const int groups = K >> G;
   constexpr int low_mask = (1 << S) - 1;
   for (int g = threadIdx.x; g < groups; g += T) {
     const int base = (g & low_mask) | ((g >> S) << (S + G));
-    const float* src = lds + lidx(base);
+    const float* src = lds + lidx<PD>(base);
     float v[1 << G];
 #pragma unroll
-    for (int k = 0; k < (1 << G); ++k) v[k] = src[lidx_c(k << S)];
+    for (int k = 0; k < (1 << G); ++k) v[k] = src[lidx<PD>(k << S)];
     butterflies<G>(v, 0, G);
-    float* dst = lds + lidx(base);
+    float* dst = lds + lidx<PD>(base);
 #pragma unroll
     for (int k = 0; k < (1 << G); ++k) {
-      dst[lidx_c(k << S)] = v[k];
+      dst[lidx<PD>(k << S)] = v[k];
       if (last) tmax = fmaxf(tmax, fabsf(v[k]));
     }
   }
@@ -115,22 +124,22 @@ __device__ __forceinline__ float pass_bits(float* lds, int K, bool last, float t
 }
 
 // Element a (slow index) of a 28-point column at base: lidx(base + a p).
-// With p = 2^J >= 256 the padding splits (base's fast part lies below bit J,
-// and a p adds whole multiples of 256), so it is lidx(base) plus the constant
-// a (p + p / 32); the column then reads from two bases, 14 rows apart, so that
-// every offset fits the LDS instructions' immediate.  Below 256 it is
-// computed per element.
-template <int J>
+// With p = 2^J at least the padding period (256 or 32) the padding splits
+// (base's fast part lies below bit J, and a p adds whole periods), so it is
+// lidx(base) plus the constant a lidx(p); the column then reads from two
+// bases, 14 rows apart, so that every offset fits the LDS instructions'
+// immediate.  Below that it is computed per element.
+template <int J, int PD>
 struct Col28 {
   static constexpr int kP = 1 << J;
-  static constexpr bool kSplit = J >= 8;
-  static constexpr int kStep = kP + kP / 32;
+  static constexpr bool kSplit = J >= (PD == 0 ? 8 : 5);
+  static constexpr int kStep = lidx<PD>(kP);
   float* b0;
   float* b1;
   int base;
   __device__ __forceinline__ Col28(float* lds, int base_) : base(base_) {
     if constexpr (kSplit) {
-      b0 = lds + lidx(base_);
+      b0 = lds + lidx<PD>(base_);
       b1 = b0 + 14 * kStep;
     } else {
       b0 = lds;
@@ -139,15 +148,15 @@ struct Col28 {
   }
   __device__ __forceinline__ float& at(int a) const {
     if constexpr (kSplit) return a < 14 ? b0[a * kStep] : b1[(a - 14) * kStep];
-    else return b0[lidx(base + a * kP)];
+    else return b0[lidx<PD>(base + a * kP)];
   }
 };
 
 // Dense 28-point stage: y[b*p + c] = sum over a = 0..27 (in order) of
 // H28[a][b] * z[a*p + c], per block and fast index c.  Outputs B0 .. B0+NB-1
 // of one column from its 28 inputs z (shared partial sums, h28_column).
-template <int NB, int B0, int J>
-__device__ __forceinline__ float dense28(const Col28<J>& col, const float* z, float tmax) {
+template <int NB, int B0, int J, int PD>
+__device__ __forceinline__ float dense28(const Col28<J, PD>& col, const float* z, float tmax) {
   h28_column<B0, NB>(z, [&](int b, float acc) __attribute__((always_inline)) {
     col.at(B0 + b) = acc;
     tmax = fmaxf(tmax, fabsf(acc));
@@ -155,7 +164,7 @@ __device__ __forceinline__ float dense28(const Col28<J>& col, const float* z, fl
   return tmax;
 }
 
-template <int T, int J>
+template <int T, int J, int PD>
 __device__ __forceinline__ float pass_28(float* lds, int K, float tmax) {
   constexpr int p = 1 << J;
   const int cols = K / 28;
@@ -165,7 +174,7 @@ __device__ __forceinline__ float pass_28(float* lds, int K, float tmax) {
     const int t = threadIdx.x;
     const bool active = t < 2 * cols;
     const int c = t % cols, half = t / cols;
-    const Col28<J> col(lds, (c >> J) * 28 * p + (c & (p - 1)));
+    const Col28<J, PD> col(lds, (c >> J) * 28 * p + (c & (p - 1)));
     float z[28];
     if (active) {
 #pragma unroll
@@ -173,17 +182,17 @@ __device__ __forceinline__ float pass_28(float* lds, int K, float tmax) {
     }
     __syncthreads();
     if (active) {
-      if (half == 0) tmax = dense28<14, 0, J>(col, z, tmax);
-      else tmax = dense28<14, 14, J>(col, z, tmax);
+      if (half == 0) tmax = dense28<14, 0, J, PD>(col, z, tmax);
+      else tmax = dense28<14, 14, J, PD>(col, z, tmax);
     }
     return tmax;
   }
   for (int c = threadIdx.x; c < cols; c += T) {
-    const Col28<J> col(lds, (c >> J) * 28 * p + (c & (p - 1)));
+    const Col28<J, PD> col(lds, (c >> J) * 28 * p + (c & (p - 1)));
     float z[28];
 #pragma unroll
     for (int a = 0; a < 28; ++a) z[a] = col.at(a);
-    tmax = dense28<28, 0, J>(col, z, tmax);
+    tmax = dense28<28, 0, J, PD>(col, z, tmax);
   }
   return tmax;
 }
@@ -320,6 +329,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
   __shared__ float red3[T / 64][3];
   float3 sums = make_float3(0.0f, 0.0f, 0.0f);
   using P = Plan<J>;
+  constexpr int PD = pad_of<F, J>();
   static_assert(P::np <= 3, "pass plan too long");
   static_assert(!FP6 || BITS == 4, "FP6 output holds 4-bit codes");
   const int mblk = (M + 31) >> 5;
@@ -349,26 +359,26 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
     }
     butterflies<3>(v, 0, P::j0);
     if (load_last) tmax = absmax8(v, tmax);
-    float4* d = reinterpret_cast<float4*>(lds + lidx(q * 8));
+    float4* d = reinterpret_cast<float4*>(lds + lidx<PD>(q * 8));
     d[0] = make_float4(v[0], v[1], v[2], v[3]);
     d[1] = make_float4(v[4], v[5], v[6], v[7]);
   }
   __syncthreads();
 
   if constexpr (P::np > 0) {
-    tmax = pass_bits<P::width(0), P::start(0), T>(lds, K, P::np == 1 && F == 1, tmax);
+    tmax = pass_bits<P::width(0), P::start(0), T, PD>(lds, K, P::np == 1 && F == 1, tmax);
     __syncthreads();
   }
   if constexpr (P::np > 1) {
-    tmax = pass_bits<P::width(1), P::start(1), T>(lds, K, P::np == 2 && F == 1, tmax);
+    tmax = pass_bits<P::width(1), P::start(1), T, PD>(lds, K, P::np == 2 && F == 1, tmax);
     __syncthreads();
   }
   if constexpr (P::np > 2) {
-    tmax = pass_bits<P::width(2), P::start(2), T>(lds, K, F == 1, tmax);
+    tmax = pass_bits<P::width(2), P::start(2), T, PD>(lds, K, F == 1, tmax);
     __syncthreads();
   }
   if constexpr (F == 28) {
-    tmax = pass_28<T, J>(lds, K, tmax);
+    tmax = pass_28<T, J, PD>(lds, K, tmax);
     __syncthreads();
   }
 
@@ -401,7 +411,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
     // so quads stay together and every quad's items exist or none do.
     for (int q0 = threadIdx.x & ~3; q0 < nchunk; q0 += T) {
       const int q = q0 + (threadIdx.x & 3);
-      const float4* src = reinterpret_cast<const float4*>(lds + lidx(q * 8));
+      const float4* src = reinterpret_cast<const float4*>(lds + lidx<PD>(q * 8));
       const float4 a = src[0], b = src[1];
       const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
       uint32_t hw[4];   // the 8 values c / 2 as packed fp16 pairs
@@ -433,7 +443,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
     return;
   }
   for (int q = threadIdx.x; q < nchunk; q += T) {
-    const float4* src = reinterpret_cast<const float4*>(lds + lidx(q * 8));
+    const float4* src = reinterpret_cast<const float4*>(lds + lidx<PD>(q * 8));
     const float4 a = src[0], b = src[1];
     const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
     if constexpr (STATS) {
@@ -456,25 +466,28 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
   }
 }
 
-size_t lds_bytes(int K) {
-  return (size_t)(K + ((K + 255) >> 8) * 8) * sizeof(float);
+size_t lds_bytes(int K, int pd) {
+  return (size_t)(K + (pd == 0 ? ((K + 255) >> 8) * 8 : ((K + 31) >> 5) * 4)) * sizeof(float);
 }
+constexpr size_t kLdsMax = 160 * 1024;
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
 hipError_t launch_one_t(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
                         float* scales, StatsArgs st, hipStream_t stream) {
   auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T, STATS, FP6>;
+  constexpr int PD = pad_of<F, J>();
   static bool attr_set = false;
   if (!attr_set) {
     // Rows above 64 KiB of LDS need the larger dynamic allocation enabled.
+    const size_t most = lds_bytes(kMaxRotateK, PD);
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)lds_bytes(kMaxRotateK));
+                              (int)(most < kLdsMax - 4096 ? most : kLdsMax - 4096));
     (void)hipGetLastError();
     attr_set = true;
   }
   const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(T), lds_bytes(K), stream, x, (int)M, K,
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(T), lds_bytes(K, PD), stream, x, (int)M, K,
                      signs, codes, scales, st);
   return hipGetLastError();
 }
@@ -489,7 +502,7 @@ constexpr size_t kOneRowLds = 80 * 1024;
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS, bool FP6>
 hipError_t launch_one(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
                       float* scales, StatsArgs st, hipStream_t stream) {
-  if (M <= kFewRows || lds_bytes(K) > kOneRowLds)
+  if (M <= kFewRows || lds_bytes(K, pad_of<F, J>()) > kOneRowLds)
     return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, signs, codes, scales, st,
                                                                   stream);
   return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, signs, codes, scales,
