@@ -198,8 +198,8 @@ typedef enum {
  * stores them).  The rotation is repeated in every workgroup, so this path
  * wins only for one or two rows of moderate K; DPTQ_DECODE_AUTO takes it for
  * N <= 16384 and either M = 1 with K <= 16384 and had_size a power of two
- * <= 8192 (or K <= 14336 and had_size = 28 * 2^j), or M = 2 with K <= 12288
- * and had_size a power of two <= 4096; and the two launches otherwise.
+ * <= 8192, or M = 2 with K <= 12288 and had_size a power of two <= 4096; and
+ * the two launches otherwise (had_size = 28 * 2^j included).
  *
  *   x, M, K, had_size, bits   as for dptq_rotate_quant; 1 <= M <= 16 (M = 0
  *            enqueues nothing), K a multiple of 128

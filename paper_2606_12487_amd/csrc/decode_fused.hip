@@ -325,14 +325,15 @@ int64_t decode_fused_lds(int64_t M, int K, HadSplit hs, int bits) {
 }
 
 // Measured on decode shapes: the repeated rotation costs less than the
-// second launch for one row of K <= 16384 with h = 2^j <= 8192, or of
-// K <= 14336 with h = 28 * 2^j, and for two rows of K <= 12288 with
-// h = 2^j <= 4096; in every case for at most 1024 workgroups (about three
-// per compute unit, so each rotates once).  More rows, longer rows or more
-// workgroups make it the slower path.
+// second launch for one row of K <= 16384 with h = 2^j <= 8192, and for two
+// rows of K <= 12288 with h = 2^j <= 4096; in every case for at most 1024
+// workgroups (about three per compute unit, so each rotates once).  More
+// rows, longer rows or more workgroups make it the slower path, and so does
+// h = 28 * 2^j since the two-launch rotation got faster (15.1 against
+// 15.7 us for one row of 14336, h = 28 x 512, N = 4096).
 bool decode_one_launch_wins(int64_t M, int K, HadSplit hs, int bits, int64_t N) {
   if (N > 16384 || decode_fused_lds(M, K, hs, bits) > kFusedLdsMax) return false;
-  if (M == 1) return hs.f == 28 ? K <= 14336 : (hs.j <= 13 && K <= 16384);
+  if (M == 1) return hs.f == 1 && hs.j <= 13 && K <= 16384;
   return M == 2 && hs.f == 1 && hs.j <= 12 && K <= 12288;
 }
 
