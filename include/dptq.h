@@ -485,14 +485,18 @@ int dptq_qlinear_fp6(const uint8_t* a_fp6, const float* a_scales, int64_t M, int
 /* Device-native weight layouts of dptq_prepack_weights. */
 typedef enum {
   DPTQ_WEIGHTS_FP6 = 1,     /* FP6 block layout: the 4-bit layers on dptq_qlinear_fp6 */
-  DPTQ_WEIGHTS_A8_ORDER = 2 /* 8-bit activation order: the 8-bit layers on dptq_qlinear_a8 */
+  DPTQ_WEIGHTS_A8_ORDER = 2, /* 8-bit activation order: the 8-bit layers on dptq_qlinear_a8 */
+  DPTQ_WEIGHTS_DECODE = 3    /* decode layout: any layer's M <= 16 GEMM on
+                                dptq_qlinear_decode_native */
 } dptq_weight_layout;
 
 /*
  * dptq_prepacked_bytes - bytes of the dptq_prepack_weights output for an
  * [N, K] weight matrix: dptq_fp6_bytes(N, K) for DPTQ_WEIGHTS_FP6 (rows padded
  * to a multiple of 32), N * K / 2 for DPTQ_WEIGHTS_A8_ORDER.  -1 for an
- * unknown layout, N < 0, or K not a multiple of 128 in [128, DPTQ_MAX_K].
+ * unknown layout, N < 0, or K not a multiple of 128 in [128, DPTQ_MAX_K];
+ * N * K / 2 for DPTQ_WEIGHTS_DECODE, which also needs N % 16 == 0 (-1
+ * otherwise).
  */
 int64_t dptq_prepacked_bytes(int64_t N, int64_t K, int32_t layout);
 
@@ -501,11 +505,15 @@ int64_t dptq_prepacked_bytes(int64_t N, int64_t K, int32_t layout);
  * output channel at 4 bits, Section 4.2; dptq_prepare_weights output) moved
  * into the layout the GEMM of their layer reads natively.  The policy of
  * Algorithm 1 step 2 / Eq. 21 fixes one activation width per layer, so each
- * weight matrix needs one layout: DPTQ_WEIGHTS_FP6 for a 4-bit layer
+ * weight matrix needs one prefill layout: DPTQ_WEIGHTS_FP6 for a 4-bit layer
  * (dptq_qlinear_fp6), DPTQ_WEIGHTS_A8_ORDER for an 8-bit layer
- * (dptq_qlinear_a8).  The codes are unchanged and so is every product: the
- * call equals dptq_pack_fp6 or dptq_pack_w4_a8 on the same arguments.  Run
- * once per weight matrix, offline.
+ * (dptq_qlinear_a8); the call then equals dptq_pack_fp6 or dptq_pack_w4_a8 on
+ * the same arguments.  DPTQ_WEIGHTS_DECODE (N % 16 == 0) is the layout of the
+ * decode GEMM at either activation width (dptq_qlinear_decode_native): per
+ * block of 16 rows and chunk of 128 k, the 64 bytes of each row's chunk as
+ * four 16-byte pieces, the 1 KiB in the order (piece, row), so that the
+ * decode GEMM streams each chunk as one contiguous KiB.  The codes are
+ * unchanged and so is every product.  Run once per weight matrix, offline.
  *
  *   w_packed device, uint8 [N, K/2] in the dptq_qlinear layout (low nibble =
  *            even k), 16-byte aligned
@@ -517,6 +525,22 @@ int64_t dptq_prepacked_bytes(int64_t N, int64_t K, int32_t layout);
  */
 int dptq_prepack_weights(const uint8_t* w_packed, int64_t N, int64_t K, int32_t layout,
                          uint8_t* w_native, void* stream);
+
+/*
+ * dptq_qlinear_decode_native - dptq_qlinear (y != NULL; a_scales and
+ * w_scales required, acc NULL) or dptq_qlinear_acc (acc != NULL; scales
+ * ignored, y NULL) for decode batches, 0 <= M <= 16 tokens (Section 2
+ * Y = X W^T, Section 4.2 scales; the decode stage of Section 4.9), on weights
+ * in DPTQ_WEIGHTS_DECODE: the same results bit for bit as dptq_qlinear on the
+ * canonical weights.  codes, a_scales, bits, K, N, y and acc as for
+ * dptq_qlinear / dptq_qlinear_acc; w_dec device, dptq_prepacked_bytes(N, K,
+ * DPTQ_WEIGHTS_DECODE) bytes, 16-byte aligned.  DPTQ_ERR_UNSUPPORTED for
+ * M > 16 or a shape outside dptq_qlinear's range, DPTQ_ERR_INVALID_ARG when
+ * not exactly one of y and acc is given.
+ */
+int dptq_qlinear_decode_native(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                               int32_t bits, const uint8_t* w_dec, const float* w_scales,
+                               int64_t N, void* y, int32_t* acc, void* stream);
 
 #ifdef __cplusplus
 }

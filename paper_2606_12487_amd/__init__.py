@@ -20,7 +20,8 @@ __all__ = ["DptqError", "lib", "library_path", "rotate_quant", "qlinear", "qline
            "LAYOUT_PACKED", "LAYOUT_FP6", "qlinear_decode_fused", "DECODE_AUTO", "DECODE_ONE_LAUNCH",
            "DECODE_TWO_LAUNCHES", "rotate_quant_range", "weight_sums", "qlinear_range",
            "qlinear_fp6_acc", "pack_w4_a8", "qlinear_a8", "prepacked_bytes", "prepack_weights",
-           "WEIGHTS_FP6", "WEIGHTS_A8_ORDER",
+           "WEIGHTS_FP6", "WEIGHTS_A8_ORDER", "WEIGHTS_DECODE", "qlinear_decode_native",
+           "qlinear_decode_native_acc",
            "EXPORTED_FUNCTIONS", "GEMM_AUTO",
            "GEMM_DECODE", "GEMM_TILE_256X128", "GEMM_TILE_192X256"]
 
@@ -38,13 +39,14 @@ EXPORTED_FUNCTIONS = ("dptq_status_string", "dptq_version", "dptq_rotate_quant",
                       "dptq_qlinear_fp6", "dptq_rotate_quant_ex", "dptq_prepare_weights_signed",
                       "dptq_qlinear_decode_fused", "dptq_rotate_quant_range",
                       "dptq_weight_sums", "dptq_qlinear_range", "dptq_pack_w4_a8",
-                      "dptq_qlinear_a8", "dptq_prepacked_bytes", "dptq_prepack_weights")
+                      "dptq_qlinear_a8", "dptq_prepacked_bytes", "dptq_prepack_weights",
+                      "dptq_qlinear_decode_native")
 
 # Code layouts of dptq_rotate_quant_ex.
 LAYOUT_PACKED, LAYOUT_FP6 = 0, 1
 
 # Device-native weight layouts of dptq_prepack_weights.
-WEIGHTS_FP6, WEIGHTS_A8_ORDER = 1, 2
+WEIGHTS_FP6, WEIGHTS_A8_ORDER, WEIGHTS_DECODE = 1, 2, 3
 
 # GEMM kernels (dptq_gemm_kernel); every kernel returns the same bits.
 GEMM_AUTO, GEMM_DECODE, GEMM_TILE_256X128, GEMM_TILE_192X256 = 0, 1, 2, 3
@@ -83,6 +85,8 @@ def lib():
         L.dptq_qlinear_acc.restype = ctypes.c_int
         L.dptq_qlinear_kernel.argtypes = [vp, vp, i64, i64, i32, vp, vp, i64, vp, vp, i32, vp]
         L.dptq_qlinear_kernel.restype = ctypes.c_int
+        L.dptq_qlinear_decode_native.argtypes = [vp, vp, i64, i64, i32, vp, vp, i64, vp, vp, vp]
+        L.dptq_qlinear_decode_native.restype = ctypes.c_int
         L.dptq_residual_dynamics.argtypes = [vp, vp, i64, i64, i32, i32, ctypes.c_float,
                                              vp, vp, vp, vp]
         L.dptq_residual_dynamics.restype = ctypes.c_int
@@ -286,14 +290,16 @@ def prepacked_bytes(N, K, layout):
     """Bytes of the prepack_weights output for [N, K] weights in `layout`."""
     n = lib().dptq_prepacked_bytes(int(N), int(K), int(layout))
     if n < 0:
-        raise ValueError(f"no layout {layout} for N={N}, K={K} (K must be a multiple of 128)")
+        raise ValueError(f"no layout {layout} for N={N}, K={K} (K must be a multiple of 128; "
+                         "the decode layout also needs N % 16 == 0)")
     return n
 
 
 def prepack_weights(w_packed, layout, out=None):
     """4-bit weights [N, K/2] in the qlinear layout -> the device-native layout
     of their layer's GEMM (WEIGHTS_FP6 for qlinear_fp6, WEIGHTS_A8_ORDER for
-    qlinear_a8), uint8 [prepacked_bytes(N, K, layout)]."""
+    qlinear_a8, WEIGHTS_DECODE for qlinear_decode_native), uint8
+    [prepacked_bytes(N, K, layout)]."""
     torch = _torch()
     _require(w_packed, "w_packed", torch.uint8)
     if w_packed.dim() != 2:
@@ -306,6 +312,48 @@ def prepack_weights(w_packed, layout, out=None):
     _check(lib().dptq_prepack_weights(_ptr(w_packed), N, K, int(layout), _ptr(out),
                                       _stream(w_packed)), "dptq_prepack_weights")
     return out
+
+
+def _decode_native_args(codes, bits, w_dec, N):
+    torch = _torch()
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    cdt = torch.uint8 if bits == 4 else torch.int8
+    _require(codes, "codes", cdt)
+    M = codes.shape[0]
+    K = codes.shape[1] * (2 if bits == 4 else 1)
+    _require(w_dec, "w_dec", torch.uint8, (prepacked_bytes(N, K, WEIGHTS_DECODE),))
+    return M, K
+
+
+def qlinear_decode_native(codes, a_scales, bits, w_dec, w_scales, y=None):
+    """qlinear for M <= 16 tokens on weights from prepack_weights(w, WEIGHTS_DECODE):
+    the same y bit for bit.  N is taken from w_scales."""
+    torch = _torch()
+    N = w_scales.shape[0]
+    M, K = _decode_native_args(codes, bits, w_dec, N)
+    _require(a_scales, "a_scales", torch.float32, (M,))
+    _require(w_scales, "w_scales", torch.float32, (N,))
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=codes.device)
+    _require(y, "y", torch.float16, (M, N))
+    _check(lib().dptq_qlinear_decode_native(_ptr(codes), _ptr(a_scales), M, K, int(bits), _ptr(w_dec),
+                                            _ptr(w_scales), N, _ptr(y), None, _stream(codes)),
+           "dptq_qlinear_decode_native")
+    return y
+
+
+def qlinear_decode_native_acc(codes, bits, w_dec, N, acc=None):
+    """The int32 accumulators [M, N] of qlinear_decode_native (exact)."""
+    torch = _torch()
+    M, K = _decode_native_args(codes, bits, w_dec, N)
+    if acc is None:
+        acc = torch.empty((M, N), dtype=torch.int32, device=codes.device)
+    _require(acc, "acc", torch.int32, (M, N))
+    _check(lib().dptq_qlinear_decode_native(_ptr(codes), None, M, K, int(bits), _ptr(w_dec), None, N,
+                                            None, _ptr(acc), _stream(codes)),
+           "dptq_qlinear_decode_native")
+    return acc
 
 
 def qlinear_a8(codes, a_scales, w_a8, w_scales, y=None, kernel=GEMM_AUTO):

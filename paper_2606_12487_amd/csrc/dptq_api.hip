@@ -232,6 +232,7 @@ int64_t dptq_prepacked_bytes(int64_t N, int64_t K, int32_t layout) {
   if (N < 0 || K < 128 || K % 128 != 0 || K > DPTQ_MAX_K) return -1;
   if (layout == DPTQ_WEIGHTS_FP6) return dptq_fp6_bytes(N, K);
   if (layout == DPTQ_WEIGHTS_A8_ORDER) return N > 0x7FFFFFF0 ? -1 : N * (K / 2);
+  if (layout == DPTQ_WEIGHTS_DECODE) return (N > 0x7FFFFFF0 || N % 16 != 0) ? -1 : N * (K / 2);
   return -1;
 }
 
@@ -239,7 +240,38 @@ int dptq_prepack_weights(const uint8_t* w_packed, int64_t N, int64_t K, int32_t 
                          uint8_t* w_native, void* stream) {
   if (layout == DPTQ_WEIGHTS_FP6) return dptq_pack_fp6(w_packed, N, K, w_native, stream);
   if (layout == DPTQ_WEIGHTS_A8_ORDER) return dptq_pack_w4_a8(w_packed, N, K, w_native, stream);
+  if (layout == DPTQ_WEIGHTS_DECODE) {
+    if (N < 0 || K < 1) return DPTQ_ERR_INVALID_ARG;
+    if (K % 128 != 0 || K > DPTQ_MAX_K || N > 0x7FFFFFF0 || N % 16 != 0) return DPTQ_ERR_UNSUPPORTED;
+    if (N == 0) return DPTQ_OK;
+    if (!w_packed || !w_native) return DPTQ_ERR_INVALID_ARG;
+    if (!aligned16(w_packed) || !aligned16(w_native)) return DPTQ_ERR_INVALID_ARG;
+    return from_hip(dptq::launch_pack_decode(w_packed, N, (int)K, w_native,
+                                             static_cast<hipStream_t>(stream)));
+  }
   return DPTQ_ERR_INVALID_ARG;
+}
+
+int dptq_qlinear_decode_native(const void* codes, const float* a_scales, int64_t M, int64_t K,
+                               int32_t bits, const uint8_t* w_dec, const float* w_scales,
+                               int64_t N, void* y, int32_t* acc, void* stream) {
+  int st = check_gemm_shape(M, K, bits, N);
+  if (st != DPTQ_OK) return st;
+  if (M > 16) return DPTQ_ERR_UNSUPPORTED;
+  if ((y == nullptr) == (acc == nullptr)) return DPTQ_ERR_INVALID_ARG;
+  if (M == 0) return DPTQ_OK;
+  if (!codes || !w_dec) return DPTQ_ERR_INVALID_ARG;
+  if (!aligned16(codes) || !aligned16(w_dec)) return DPTQ_ERR_INVALID_ARG;
+  if (y) {
+    if (!a_scales || !w_scales) return DPTQ_ERR_INVALID_ARG;
+    if (!aligned16(a_scales) || !aligned16(w_scales) || !aligned16(y)) return DPTQ_ERR_INVALID_ARG;
+  } else if (!aligned16(acc)) {
+    return DPTQ_ERR_INVALID_ARG;
+  }
+  return from_hip(dptq::launch_qlinear_decode_native(codes, y ? a_scales : nullptr, M, (int)K, bits,
+                                                     w_dec, y ? w_scales : nullptr, N, y,
+                                                     y ? nullptr : acc,
+                                                     static_cast<hipStream_t>(stream)));
 }
 
 int dptq_rotate_quant_fp6(const void* x, int64_t M, int64_t K, int32_t had_size, uint8_t* out,

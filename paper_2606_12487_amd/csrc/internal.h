@@ -64,6 +64,17 @@ hipError_t launch_qlinear(const void* codes, const float* a_scales, int64_t M,
 // ones; K % 8 == 0).
 hipError_t launch_pack_w4_a8(const uint8_t* w_packed, int64_t N, int K, uint8_t* out,
                              hipStream_t stream);
+// 4-bit weights [N, K/2] (canonical order, N % 16 == 0, K % 128 == 0) -> the
+// decode layout of the M <= 16 GEMM (same size): per 16-row block and 128-k
+// chunk, 1 KiB holding piece g (bytes 16 g .. 16 g + 15 of the chunk) of
+// row r at position g * 16 + r, in units of 16 bytes.
+hipError_t launch_pack_decode(const uint8_t* w_packed, int64_t N, int K, uint8_t* out,
+                              hipStream_t stream);
+// The decode GEMM (1 <= M <= 16) + epilogue, or the int32 accumulators when
+// out_acc != nullptr, against weights in the decode layout.
+hipError_t launch_qlinear_decode_native(const void* codes, const float* a_scales, int64_t M, int K,
+                                        int bits, const uint8_t* w_dec, const float* w_scales,
+                                        int64_t N, void* y, int32_t* out_acc, hipStream_t stream);
 // W4A8 GEMM + epilogue against weights in the 8-bit activation order; the
 // kernel choice as for launch_qlinear.
 hipError_t launch_qlinear_a8(const void* codes, const float* a_scales, int64_t M, int K,

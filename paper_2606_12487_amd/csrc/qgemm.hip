@@ -1000,8 +1000,11 @@ constexpr int kDecBatch = 4;
 
 // ZP: the range quantizer's zero-point correction in the epilogue,
 // acc + (2^(BITS-1) - a_zeros[m]) * w_sums[n] (exact int32), before the
-// dequantization.
-template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false, int NB = 1>
+// dequantization.  WDEC: weights in the decode layout (below), where the
+// 16 rows x 64 bytes of a block's 128-k chunk are one contiguous KiB in lane
+// order, so each load instruction streams 1 KiB instead of 16 runs of 64
+// bytes 8 K bytes apart.
+template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false, int NB = 1, bool WDEC = false>
 __global__ void __launch_bounds__(kDecWaves * 64)
 qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
              const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
@@ -1019,7 +1022,10 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
   const bool mvalid = fr < M;
 
   const size_t wrow = (size_t)K / 2;
-  const uint8_t* wp = w_packed + (size_t)(n0 + fr) * wrow + fg * 16;
+  // Chunk ck of weight block nb (16 rows) at wp + nb * 16 * wrow + ck * kChunk.
+  constexpr size_t kChunk = WDEC ? 1024 : 64;
+  const uint8_t* wp = WDEC ? w_packed + (size_t)n0 * wrow + lane * 16
+                           : w_packed + (size_t)(n0 + fr) * wrow + fg * 16;
   const size_t arow = BITS == 4 ? (size_t)K / 2 : (size_t)K;
   const uint8_t* ap = a_codes + (size_t)(mvalid ? fr : 0) * arow + (BITS == 4 ? fg * 16 : fg * 32);
 
@@ -1034,7 +1040,7 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
       const bool ok = ck < c_end;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        wv[nb][b] = ok ? *reinterpret_cast<const uint4*>(wp + (size_t)nb * 16 * wrow + (size_t)ck * 64)
+        wv[nb][b] = ok ? *reinterpret_cast<const uint4*>(wp + (size_t)nb * 16 * wrow + (size_t)ck * kChunk)
                        : make_uint4(0, 0, 0, 0);
       if (BITS == 4) {
         av[b] = (ok && mvalid) ? *reinterpret_cast<const uint4*>(ap + (size_t)ck * 64)
@@ -1110,22 +1116,39 @@ int decode_blocks(int64_t M, int64_t N, int bits, int cus) {
   return 1;
 }
 
-template <int BITS, bool ACC_OUT, bool WA8, bool ZP>
+template <int BITS, bool ACC_OUT, bool WA8, bool ZP, bool WDEC = false>
 void launch_decode(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
                    const float* ws, int64_t N, __half* y, int32_t* acc, const int32_t* az,
                    const int32_t* wsum, hipStream_t stream) {
   switch (decode_blocks(M, N, BITS, device_cus())) {
     case 2:
-      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 2>), dim3((unsigned)(N / 32)),
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 2, WDEC>), dim3((unsigned)(N / 32)),
                          dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
                          az, wsum);
       break;
     default:
-      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 1>), dim3((unsigned)(N / 16)),
+      hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 1, WDEC>), dim3((unsigned)(N / 16)),
                          dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
                          az, wsum);
       break;
   }
+}
+
+// Canonical 4-bit weights [N, K/2] -> the decode layout: block b of 16 rows,
+// chunk c of 128 k, piece g of 16 bytes, row r of the block -> the 16 bytes
+// at ((b * (K / 128) + c) * 4 + g) * 256 + r * 16, copied from row 16 b + r,
+// bytes 64 c + 16 g .. 64 c + 16 g + 15.  One 16-byte piece per thread.
+__global__ void __launch_bounds__(256)
+pack_decode_kernel(const uint4* __restrict__ w, int64_t npieces, int K, uint4* __restrict__ out) {
+  const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (o >= npieces) return;
+  const int64_t per_block = (int64_t)(K / 128) * 64;     // 16-byte pieces per 16-row block
+  const int64_t b = o / per_block;
+  const int rem = (int)(o - b * per_block);
+  const int c = rem >> 6, l = rem & 63;
+  const int r = l & 15, g = l >> 4;
+  const int64_t row_pieces = K / 32;                     // 16-byte pieces per row
+  out[o] = w[(16 * b + r) * row_pieces + 4 * c + g];
 }
 
 // Weights in the 8-bit activation order: dword g of a row holds k = 8g ..
@@ -1283,6 +1306,39 @@ hipError_t launch_pack_w4_a8(const uint8_t* w_packed, int64_t N, int K, uint8_t*
   if (ndw == 0) return hipSuccess;
   hipLaunchKernelGGL(pack_w4_a8_kernel, dim3((unsigned)((ndw + 255) / 256)), dim3(256), 0, stream,
                      reinterpret_cast<const uint32_t*>(w_packed), ndw, reinterpret_cast<uint32_t*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_decode(const uint8_t* w_packed, int64_t N, int K, uint8_t* out,
+                              hipStream_t stream) {
+  const int64_t npieces = N * (K / 32);
+  if (npieces == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_decode_kernel, dim3((unsigned)((npieces + 255) / 256)), dim3(256), 0,
+                     stream, reinterpret_cast<const uint4*>(w_packed), npieces, K,
+                     reinterpret_cast<uint4*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_qlinear_decode_native(const void* codes, const float* a_scales, int64_t M, int K,
+                                        int bits, const uint8_t* w_dec, const float* w_scales,
+                                        int64_t N, void* y, int32_t* out_acc, hipStream_t stream) {
+  if (M == 0) return hipSuccess;
+  const uint8_t* a = static_cast<const uint8_t*>(codes);
+  __half* yh = static_cast<__half*>(y);
+  if (out_acc) {
+    if (bits == 4)
+      launch_decode<4, true, false, false, true>(a, nullptr, M, K, w_dec, nullptr, N, nullptr,
+                                                 out_acc, nullptr, nullptr, stream);
+    else
+      launch_decode<8, true, false, false, true>(a, nullptr, M, K, w_dec, nullptr, N, nullptr,
+                                                 out_acc, nullptr, nullptr, stream);
+  } else if (bits == 4) {
+    launch_decode<4, false, false, false, true>(a, a_scales, M, K, w_dec, w_scales, N, yh, nullptr,
+                                                nullptr, nullptr, stream);
+  } else {
+    launch_decode<8, false, false, false, true>(a, a_scales, M, K, w_dec, w_scales, N, yh, nullptr,
+                                                nullptr, nullptr, stream);
+  }
   return hipGetLastError();
 }
 

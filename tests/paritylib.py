@@ -175,3 +175,14 @@ def assert_acc(got, ref, what):
         f"({np.unique(rows).size} rows, 256-row tiles {np.unique(rows // 256)[:12]}), "
         f"cols {np.unique(cols)[:12]} ({np.unique(cols).size} cols, 192-col tiles "
         f"{np.unique(cols // 192)[:12]}); got {g[bad][:6]} want {ref[bad][:6]}")
+
+
+def decode_layout_ref(w_packed):
+    """The decode layout written out from its definition: for 16-row block b,
+    128-k chunk c, 16-byte piece g of the chunk and row r of the block, the
+    piece sits at 16-byte position ((b * (K / 128) + c) * 4 + g) * 16 + r."""
+    w = np.ascontiguousarray(w_packed)
+    N, half = w.shape
+    K = half * 2
+    pieces = w.reshape(N // 16, 16, K // 128, 4, 16)        # [b, r, c, g, byte]
+    return np.ascontiguousarray(pieces.transpose(0, 2, 3, 1, 4)).reshape(-1)

@@ -263,13 +263,31 @@ def test_prepack_weights_validation(L):
     assert L.dptq_prepacked_bytes(33, 256, 0) == -1            # no such layout
     assert L.dptq_prepacked_bytes(33, 200, 2) == -1            # K % 128 != 0
     assert L.dptq_prepacked_bytes(-1, 256, 1) == -1
-    for layout in (1, 2):
-        assert L.dptq_prepack_weights(FAKE, 4, 192, layout, FAKE, NULL) == UNSUPPORTED
-        assert L.dptq_prepack_weights(MISALIGNED, 4, 256, layout, FAKE, NULL) == INVALID
-        assert L.dptq_prepack_weights(FAKE, 4, 256, layout, NULL, NULL) == INVALID
+    assert L.dptq_prepacked_bytes(32, 256, 3) == 32 * 128       # decode layout
+    assert L.dptq_prepacked_bytes(33, 256, 3) == -1            # N % 16 != 0
+    for layout in (1, 2, 3):
+        assert L.dptq_prepack_weights(FAKE, 16, 192, layout, FAKE, NULL) == UNSUPPORTED
+        assert L.dptq_prepack_weights(MISALIGNED, 16, 256, layout, FAKE, NULL) == INVALID
+        assert L.dptq_prepack_weights(FAKE, 16, 256, layout, NULL, NULL) == INVALID
         assert L.dptq_prepack_weights(NULL, 0, 256, layout, NULL, NULL) == OK   # nothing to do
+    assert L.dptq_prepack_weights(FAKE, 4, 256, 3, FAKE, NULL) == UNSUPPORTED  # N % 16 != 0
     assert L.dptq_prepack_weights(FAKE, 4, 256, 0, FAKE, NULL) == INVALID
-    assert L.dptq_prepack_weights(FAKE, 4, 256, 3, FAKE, NULL) == INVALID
+    assert L.dptq_prepack_weights(FAKE, 16, 256, 4, FAKE, NULL) == INVALID
+
+
+def test_decode_native_validation(L):
+    def dn(codes=FAKE, a_s=FAKE, M=4, K=1024, bits=4, w=FAKE, w_s=FAKE, N=256, y=FAKE, acc=NULL):
+        return L.dptq_qlinear_decode_native(codes, a_s, M, K, bits, w, w_s, N, y, acc, NULL)
+    assert dn(M=17) == UNSUPPORTED                 # decode batches only
+    assert dn(K=1000) == UNSUPPORTED
+    assert dn(N=40) == UNSUPPORTED
+    assert dn(bits=6) == INVALID
+    assert dn(acc=FAKE) == INVALID                 # both outputs
+    assert dn(y=NULL) == INVALID                   # neither output
+    assert dn(w=MISALIGNED) == INVALID
+    assert dn(a_s=NULL) == INVALID
+    assert dn(codes=NULL) == INVALID
+    assert dn(M=0) == OK                           # nothing to do
 
 
 def test_a8order_entry_points_validation(L):
