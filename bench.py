@@ -195,10 +195,10 @@ class Stack:
     4-bit) and pre-packed into the layout of the GEMM that runs the layer's
     bits: FP6 for a 4-bit layer, the 8-bit activation order for an 8-bit one.
     `fp6_all` / `a8_all` pack every layer into that layout as well (to run
-    other policies on the same weights); `canonical` keeps the canonical codes
-    (for decode)."""
+    other policies on the same weights); `decode` also keeps every layer's codes
+    in the decode layout (for decode batches)."""
 
-    def __init__(self, torch, dptq, name, M, bits, fp6_all=False, a8_all=False, canonical=False):
+    def __init__(self, torch, dptq, name, M, bits, fp6_all=False, a8_all=False, decode=False):
         import workloads
         self.torch, self.dptq = torch, dptq
         dev = torch.device("cuda:0")
@@ -206,9 +206,9 @@ class Stack:
         self.name, self.M, self.L, self.lins = name, M, cfg["L"], cfg["linears"]
         self.bits = list(bits)
         gen = torch.Generator(device=dev)
-        self.fp6, self.a8, self.canon, self.ws = [], [], [], []
+        self.fp6, self.a8, self.dec, self.ws = [], [], [], []
         for l in range(self.L):
-            f6, a8, can, wsl = [], [], [], []
+            f6, a8, dec, wsl = [], [], [], []
             for i, (_, K, N, h) in enumerate(self.lins):
                 gen.manual_seed(cfg["seed"] * 1000003 + l * 16 + i)
                 w = torch.randn((N, K), device=dev, generator=gen, dtype=torch.float32)
@@ -219,12 +219,12 @@ class Stack:
                 f6.append(dptq.prepack_weights(wp, dptq.WEIGHTS_FP6) if fp6_all or b == 4 else None)
                 a8.append(dptq.prepack_weights(wp, dptq.WEIGHTS_A8_ORDER).view(N, K // 2)
                           if a8_all or b == 8 else None)
-                can.append(wp if canonical else None)
+                dec.append(dptq.prepack_weights(wp, dptq.WEIGHTS_DECODE) if decode else None)
                 wsl.append(ws)
                 del wp
             self.fp6.append(f6)
             self.a8.append(a8)
-            self.canon.append(can)
+            self.dec.append(dec)
             self.ws.append(wsl)
         self.X = [torch.from_numpy(workloads.stack_layer_input(name, self.L // 2, n, M=M)).to(dev)
                   for n, *_ in self.lins]
@@ -274,9 +274,8 @@ class Stack:
                         events.append((kname, lin, e0, e1))
 
     def decode_launches(self, bits, X):
-        """One pass at decode size: every linear through the decode entry point
-        from fp16 x (its automatic choice of one launch or two), on the
-        canonical weights."""
+        """One pass at decode size: every linear from fp16 x, rotate+quantize
+        then the decode GEMM on the decode weight layout."""
         dptq = self.dptq
         M = X[0].shape[0]
         for l in range(self.L):
@@ -285,8 +284,8 @@ class Stack:
                 dt = self.torch.uint8 if b == 4 else self.torch.int8
                 codes = self.cbuf[: M * K * b // 8].view(dt).view(M, K * b // 8)
                 y = self.ybuf[: M * N].view(M, N)
-                dptq.qlinear_decode_fused(X[i], h, b, self.canon[l][i], self.ws[l][i], y, codes,
-                                          self.sbuf[:M], mode=dptq.DECODE_AUTO)
+                dptq.rotate_quant(X[i], h, b, codes, self.sbuf[:M])
+                dptq.qlinear_decode_native(codes, self.sbuf[:M], b, self.dec[l][i], self.ws[l][i], y)
 
 
 def time_headline(torch, dptq, args):
@@ -296,7 +295,7 @@ def time_headline(torch, dptq, args):
     mask = workloads.layer_mask(L, 4, cfg["mask_seed"])
     policy = lambda: dptq.layer_policy(L, mask)          # a1: host lookup, every step
     t0 = time.perf_counter()
-    st = Stack(torch, dptq, HEADLINE, M, policy(), fp6_all=True, canonical=True)
+    st = Stack(torch, dptq, HEADLINE, M, policy(), fp6_all=True, decode=True)
     setup_s = time.perf_counter() - t0
     progress(f"headline stack ready ({setup_s:.1f} s)")
 
@@ -429,6 +428,8 @@ def single_linear(torch, dptq, name, M, copies_bytes=300 << 20):
         if K % 128 == 0 and M > 16 else None
     w8s = [dptq.prepack_weights(wp, dptq.WEIGHTS_A8_ORDER).view(N, K // 2) for _ in range(R)] \
         if K % 128 == 0 else None
+    wds = [dptq.prepack_weights(wp, dptq.WEIGHTS_DECODE) for _ in range(R)] \
+        if K % 128 == 0 and M <= 16 else None
     y = torch.empty((M, N), dtype=torch.float16, device=dev)
     out = {"M": M, "K": K, "N": N, "had_size": h}
     n = 24
@@ -456,6 +457,15 @@ def single_linear(torch, dptq, name, M, copies_bytes=300 << 20):
         g = graph_time(torch, [(lambda i: (lambda: dptq.qlinear(codes, scales, bits, wps[i % R], ws, y)))(i)
                                for i in range(n)])
         out[f"a{bits}_int8"] = rec(k1, g, bits, "int8")
+        if wds is not None:   # decode batches: the decode weight layout, GEMM and from fp16 x
+            gd = graph_time(torch, [(lambda i: (lambda: dptq.qlinear_decode_native(
+                codes, scales, bits, wds[i % R], ws, y)))(i) for i in range(n)])
+            out[f"a{bits}_decode_layout"] = rec(k1, gd, bits, "int8")
+            xd = graph_time(torch, [(lambda i: (lambda: (
+                dptq.rotate_quant(xs[i % R], h, bits, codes, scales),
+                dptq.qlinear_decode_native(codes, scales, bits, wds[i % R], ws, y))))(i)
+                for i in range(n)])
+            out[f"a{bits}_decode_layout_from_x_us"] = round(xd, 2)
         if bits == 8 and w8s is not None:
             g8 = graph_time(torch, [(lambda i: (lambda: dptq.qlinear_a8(codes, scales, w8s[i % R], ws, y)))(i)
                                     for i in range(n)])
@@ -502,8 +512,9 @@ def stack_7b(torch, dptq):
 
 
 def decode_70b(torch, st, bits):
-    """The headline stack at M = 8 decode (every linear from fp16 x through the
-    decode entry point), one graph replay per pass."""
+    """The headline stack at M = 8 decode (every linear from fp16 x:
+    rotate+quantize, then the decode GEMM on the decode weight layout), one
+    graph replay per pass."""
     import workloads
     dev = torch.device("cuda:0")
     X = [torch.from_numpy(workloads.stack_layer_input(HEADLINE, st.L // 2, n, M=8)).to(dev)
