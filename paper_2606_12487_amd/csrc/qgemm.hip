@@ -1004,7 +1004,11 @@ constexpr int kDecBatch = 4;
 // 16 rows x 64 bytes of a block's 128-k chunk are one contiguous KiB in lane
 // order, so each load instruction streams 1 KiB instead of 16 runs of 64
 // bytes 8 K bytes apart.
-template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false, int NB = 1, bool WDEC = false>
+// BATCH: chunks per wavefront in flight (kDecBatch, or 8 where a wavefront
+// streams many chunks and the grid is at most one workgroup per compute
+// unit: decode_batch).
+template <int BITS, bool ACC_OUT, bool ZP = false, bool WA8 = false, int NB = 1, bool WDEC = false,
+          int BATCH = kDecBatch>
 __global__ void __launch_bounds__(kDecWaves * 64)
 qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_scales,
              const uint8_t* __restrict__ w_packed, const float* __restrict__ w_scales,
@@ -1032,10 +1036,10 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
   v4i acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = v4i{0, 0, 0, 0};
-  for (int c = c_begin; c < c_end; c += kDecBatch) {
-    uint4 wv[NB][kDecBatch], av[kDecBatch], av2[kDecBatch];
+  for (int c = c_begin; c < c_end; c += BATCH) {
+    uint4 wv[NB][BATCH], av[BATCH], av2[BATCH];
 #pragma unroll
-    for (int b = 0; b < kDecBatch; ++b) {
+    for (int b = 0; b < BATCH; ++b) {
       const int ck = c + b;
       const bool ok = ck < c_end;
 #pragma unroll
@@ -1053,7 +1057,7 @@ qgemm_decode(const uint8_t* __restrict__ a_codes, const float* __restrict__ a_sc
       }
     }
 #pragma unroll
-    for (int b = 0; b < kDecBatch; ++b) {
+    for (int b = 0; b < BATCH; ++b) {
       v4i b0, b1;
       if (BITS == 4) {
         b0 = op_from_nibbles(av[b].x, av[b].y);
@@ -1116,11 +1120,30 @@ int decode_blocks(int64_t M, int64_t N, int bits, int cus) {
   return 1;
 }
 
+// Eight chunks in flight instead of four: measured faster (graph-replayed,
+// decode layout) where a wavefront streams at least 12 chunks, the grid is at
+// most one workgroup per compute unit and M <= 4 (LLaMA-3-8B down, K = 14336,
+// N = 4096: M = 1 A4 7.90 -> 7.25 us, M = 4 A4 8.30 -> 7.40 us, M = 1 A8
+// 8.60 -> 8.35 us), and slower with fewer chunks or more workgroups (K = 4096,
+// N = 12288, M = 1: 6.53 -> 8.25 us; K = 8192, N = 57344, M = 8: 43.4 ->
+// 48.0 us at A8).
+bool decode_batch8(int64_t M, int K, int64_t N, int cus) {
+  return M <= 4 && K / 128 >= 12 * kDecWaves && N / 16 <= cus;
+}
+
 template <int BITS, bool ACC_OUT, bool WA8, bool ZP, bool WDEC = false>
 void launch_decode(const uint8_t* a, const float* as, int64_t M, int K, const uint8_t* w,
                    const float* ws, int64_t N, __half* y, int32_t* acc, const int32_t* az,
                    const int32_t* wsum, hipStream_t stream) {
-  switch (decode_blocks(M, N, BITS, device_cus())) {
+  const int cus = device_cus();
+  const int nb = decode_blocks(M, N, BITS, cus);
+  if (nb == 1 && decode_batch8(M, K, N, cus)) {
+    hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 1, WDEC, 8>), dim3((unsigned)(N / 16)),
+                       dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc, az,
+                       wsum);
+    return;
+  }
+  switch (nb) {
     case 2:
       hipLaunchKernelGGL((qgemm_decode<BITS, ACC_OUT, ZP, WA8, 2, WDEC>), dim3((unsigned)(N / 32)),
                          dim3(kDecWaves * 64), 0, stream, a, as, w, ws, (int)M, (int)N, K, y, acc,
