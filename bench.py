@@ -44,6 +44,8 @@ METRIC = "W4A4/W4A8 qlinear TOPS (rotate+quant+GEMM), % int8 MFMA peak; decode G
 HEADLINE = "llama2_70b_layer"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_fp6_llama2_70b_stack.txt")
 TRAFFIC_SOURCE = os.path.join(ROOT, "paper_2606_12487_amd", "csrc", "qgemm_fp6.hip")
+DECODE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_qgemm_decode_llama2_70b_M8.txt")
+DECODE_TRAFFIC_SOURCE = os.path.join(ROOT, "paper_2606_12487_amd", "csrc", "qgemm.hip")
 
 
 def parse():
@@ -58,7 +60,7 @@ def parse():
                    help="time only the headline stack (no other workloads)")
     p.add_argument("--extended", action="store_true",
                    help="also time the fused decode paths, the range quantizer, calibration and KV4")
-    p.add_argument("--only", choices=["rq6", "gemm6", "rq8", "gemm8", "copy"],
+    p.add_argument("--only", choices=["rq6", "gemm6", "rq8", "gemm8", "copy", "decode"],
                    help="launch one kernel family of the headline step --steps times at every "
                         "linear shape, nothing timed (for counter runs); copy: a 256 MiB device copy")
     return p.parse_args()
@@ -77,20 +79,23 @@ def source_digest(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic():
-    """Mean HBM bytes per launch of the headline's FP6 GEMM from the committed
-    counter summary, or None when it is missing or was taken on other sources."""
-    if not os.path.exists(TRAFFIC_FILE):
+def measured_traffic(path=None, source=None, key="hbm_bytes_per_launch"):
+    """A figure of a committed counter summary (by default the mean HBM bytes
+    per launch of the headline's FP6 GEMM), or None when the file is missing or
+    was taken on other sources of the kernel."""
+    path = path or TRAFFIC_FILE
+    source = source or TRAFFIC_SOURCE
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("source_sha256_16") != source_digest(TRAFFIC_SOURCE):
+    if kv.get("source_sha256_16") != source_digest(source):
         return None
     try:
-        return int(float(kv["hbm_bytes_per_launch"]))
+        return float(kv[key]) if key == "traffic_over_algorithmic" else int(float(kv[key]))
     except (KeyError, ValueError):
         return None
 
@@ -522,7 +527,12 @@ def decode_70b(torch, st, bits):
     ms = graph_time(torch, [lambda: st.decode_launches(bits, X)], reps=3) / 1e3
     return {"M": 8, "layers": st.L, "ms": round(ms, 3),
             "weight_GB/s": round(st.weight_bytes() / (ms * 1e-3) / 1e9, 1),
-            "frac_of_hbm_peak": round(st.weight_bytes() / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+            "frac_of_hbm_peak": round(st.weight_bytes() / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            # HBM bytes of the decode GEMM over its algorithmic bytes, from the
+            # committed counter summary of `bench.py --only decode` (None when
+            # that summary was taken on other sources of the kernel)
+            "gemm_traffic_over_algorithmic": measured_traffic(
+                DECODE_TRAFFIC_FILE, DECODE_TRAFFIC_SOURCE, "traffic_over_algorithmic")}
 
 
 def time_extended(torch, dptq):
@@ -588,6 +598,9 @@ def run_only(torch, dptq, args):
         torch.cuda.synchronize()
         print(json.dumps({"only": "copy", "bytes_per_launch": n}))
         return
+    if args.only == "decode":
+        run_only_decode(torch, dptq, args)
+        return
     import workloads
     cfg = workloads.CONFIGS[HEADLINE]
     M = cfg["M"]
@@ -633,6 +646,44 @@ def run_only(torch, dptq, args):
     torch.cuda.synchronize()
     print(json.dumps({"only": args.only, "launches_per_shape": args.steps,
                       "shapes": [[M, K, N] for _, K, N, _ in lins]}))
+
+
+def run_only_decode(torch, dptq, args):
+    """The headline stack's four linears at M = 8 decode, A4: rotate+quantize
+    from fp16 x, then the decode GEMM on the decode weight layout, --steps
+    times in a fixed cycle over the four shapes, each shape's weights cycling
+    through copies beyond the Infinity Cache (rocprofv3 kernel trace and
+    counter passes; nothing timed here)."""
+    import workloads
+    dev = torch.device("cuda:0")
+    cfg = workloads.CONFIGS[HEADLINE]
+    lins, M, bits = cfg["linears"], 8, 4
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2)
+    X = [torch.from_numpy(workloads.stack_layer_input(HEADLINE, 40, n, M=M)).to(dev) for n, *_ in lins]
+    W = []
+    for _, K, N, _ in lins:
+        copies = max(2, -(-(600 << 20) // (N * K // 2)))
+        ws = []
+        for _ in range(copies):
+            wp = torch.randint(0, 256, (N, K // 2), dtype=torch.uint8, device=dev, generator=gen)
+            ws.append(dptq.prepack_weights(wp, dptq.WEIGHTS_DECODE))
+            del wp
+        W.append((ws, torch.full((N,), 1e-5, device=dev)))
+    codes = [torch.empty((M, K // 2), dtype=torch.uint8, device=dev) for _, K, _, _ in lins]
+    s = torch.empty(M, dtype=torch.float32, device=dev)
+    ys = [torch.empty((M, N), dtype=torch.float16, device=dev) for _, _, N, _ in lins]
+    torch.cuda.synchronize()
+    for step in range(args.steps):
+        for i, (_, K, N, h) in enumerate(lins):
+            dptq.rotate_quant(X[i], h, bits, codes[i], s)
+            wcopies, wsc = W[i]
+            dptq.qlinear_decode_native(codes[i], s, bits, wcopies[step % len(wcopies)], wsc, ys[i])
+    torch.cuda.synchronize()
+    print(json.dumps({"only": "decode", "launches_per_shape": args.steps, "M": M, "bits": bits,
+                      "shapes": [[M, K, N] for _, K, N, _ in lins],
+                      "gemm_algorithmic_bytes": [N * K // 2 + 4 * N + M * K * bits // 8 + 4 * M + 2 * M * N
+                                                 for _, K, N, _ in lins]}))
 
 
 # ---------------------------------------------------------------------------

@@ -5,7 +5,7 @@
         COPY_FETCH_CSV COPY_WRITE_CSV --kernel SUBSTR --source FILE \
         --algorithmic-bytes B [--reduce mean|median] [--title T] [--command C]
     python -m paper_2606_12487_amd.rocprof_summary trace TRACE_CSV --kernel SUBSTR \
-        --first N [--title T] [--command C]
+        --first N [--labels a,b,c] [--bytes B1,B2,B3] [--title T] [--command C]
     python -m paper_2606_12487_amd.rocprof_summary counters CSV [CSV ...] --kernel SUBSTR \
         --labels a,b,c [--skip N] [--title T] [--command C]
 
@@ -17,7 +17,10 @@ known-bytes / counted-bytes of the copy, and prints HBM bytes per launch
 together with the kernel source digest they belong to.  `trace` reads the
 per-dispatch kernel trace and prints the mean duration of one kernel over its
 first N dispatches (a benchmark's headline launches, which come first) and
-over all of them.  `counters` reads counter passes of a run that launches a
+over all of them; with --labels, the dispatches of a kernel launched at
+several shapes in a fixed cycle are also averaged per position of the cycle,
+and with --bytes (one figure per label) each average is also given as GB/s.
+`counters` reads counter passes of a run that launches a
 kernel at several shapes in a fixed cycle (after N other dispatches of it)
 and prints each counter's mean per dispatch for each shape of the cycle.
 """
@@ -66,7 +69,7 @@ def _counter(path, counter, kernel, reduce="median"):
     return f(vals), len(vals)
 
 
-def trace(path, kernel, first, title, command):
+def trace(path, kernel, first, title, command, labels=None, nbytes=None):
     rows = [r for r in _rows(path) if kernel in r["Kernel_Name"]]
     if not rows:
         raise SystemExit(f"no dispatches of kernels matching {kernel!r} in {path}")
@@ -83,6 +86,14 @@ def trace(path, kernel, first, title, command):
             f"average_us_first: {statistics.mean(head):.2f}",
             f"min_us_first: {min(head):.2f}",
             f"max_us_first: {max(head):.2f}"]
+    if labels:
+        out.append("position | dispatches | average_us | min_us" + (" | GB/s" if nbytes else ""))
+        for k, lab in enumerate(labels):
+            d = dur[k::len(labels)]
+            line = f"{lab} | {len(d)} | {statistics.mean(d):.2f} | {min(d):.2f}"
+            if nbytes:
+                line += f" | {nbytes[k] / (statistics.mean(d) * 1e-6) / 1e9:.1f}"
+            out.append(line)
     return "\n".join(out)
 
 
@@ -168,6 +179,8 @@ def main(argv=None):
     r.add_argument("csv")
     r.add_argument("--kernel", required=True)
     r.add_argument("--first", type=int, required=True)
+    r.add_argument("--labels", default="")
+    r.add_argument("--bytes", default="")
     r.add_argument("--title", default="")
     r.add_argument("--command", default="")
     c = sub.add_parser("counters")
@@ -184,7 +197,9 @@ def main(argv=None):
     if a.cmd == "stats":
         print(stats(a.csv, a.title, a.command, a.top))
     elif a.cmd == "trace":
-        print(trace(a.csv, a.kernel, a.first, a.title, a.command))
+        labels = a.labels.split(",") if a.labels else None
+        nbytes = [float(b) for b in a.bytes.split(",")] if a.bytes else None
+        print(trace(a.csv, a.kernel, a.first, a.title, a.command, labels, nbytes))
     else:
         print(traffic(a, a.title, a.command))
 

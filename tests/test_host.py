@@ -36,6 +36,12 @@ def test_bench_traffic_is_tied_to_the_kernel_source(tmp_path, monkeypatch):
     assert bench.measured_traffic() == 123
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.txt"))
     assert bench.measured_traffic() is None
+    # the decode GEMM's summary is tied to the decode kernel's source the same way
+    dec = bench.measured_traffic(bench.DECODE_TRAFFIC_FILE, bench.DECODE_TRAFFIC_SOURCE,
+                                 "traffic_over_algorithmic")
+    assert dec is None or 0.9 < dec < 3.0
+    assert bench.measured_traffic(str(fake), bench.DECODE_TRAFFIC_SOURCE,
+                                  "traffic_over_algorithmic") is None
 
 
 def test_entry_module_has_build_and_smoke():
