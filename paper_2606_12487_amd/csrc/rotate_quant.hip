@@ -323,7 +323,8 @@ struct Plan {
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
 __global__ void __launch_bounds__(T)
 rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __restrict__ signs,
-                    uint8_t* __restrict__ codes, float* __restrict__ scales, StatsArgs st) {
+                    uint8_t* __restrict__ codes, float* __restrict__ scales, StatsArgs st,
+                    int touch_stride) {
   extern __shared__ float lds[];
   __shared__ float red[T / 64];
   __shared__ float red3[T / 64][3];
@@ -334,6 +335,17 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
   static_assert(!FP6 || BITS == 4, "FP6 output holds 4-bit codes");
   const int mblk = (M + 31) >> 5;
   const int row = FP6 ? fp6_row(blockIdx.x, mblk * 32) : (int)blockIdx.x;
+  // The row of workgroup blockIdx.x + touch_stride (0: none), which the
+  // dispatcher, dealing workgroups to the eight XCDs in turn, sends to this
+  // XCD once a compute unit frees up.
+  int next_row = -1;
+  if (touch_stride > 0) {
+    const int nb = (int)blockIdx.x + touch_stride;
+    if (nb < (int)gridDim.x) {
+      const int nr = FP6 ? fp6_row(nb, mblk * 32) : nb;
+      next_row = nr < M ? nr : -1;
+    }
+  }
   if constexpr (FP6) {
     if (row >= M) {   // padding row of the last block: zero codes
       for (int q = threadIdx.x; q < K / 32; q += T) {
@@ -364,6 +376,18 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
     d[1] = make_float4(v[4], v[5], v[6], v[7]);
   }
   __syncthreads();
+  // With one workgroup per compute unit the rows of a round load together
+  // and nothing hides that burst.  So, once this row is staged, touch one
+  // dword in every 64 bytes of the next row this XCD will take: it is in the
+  // L2 when its workgroup starts.  The value is only consumed (by an empty
+  // asm) when the row is done, so the load never stalls this row.
+  uint32_t touch = 0;
+  if (next_row >= 0) {
+    constexpr int kStep = 64 / (int)sizeof(Tin);
+    const Tin* xn = x + (size_t)next_row * K;
+    for (int e = threadIdx.x * kStep; e < K; e += T * kStep)
+      touch ^= *reinterpret_cast<const uint32_t*>(xn + e);
+  }
 
   if constexpr (P::np > 0) {
     tmax = pass_bits<P::width(0), P::start(0), T, PD>(lds, K, P::np == 1 && F == 1, tmax);
@@ -440,6 +464,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
         *reinterpret_cast<uint2*>(d) = make_uint2(lo, hi);
       }
     }
+    asm volatile("" : : "v"(touch));
     return;
   }
   for (int q = threadIdx.x; q < nchunk; q += T) {
@@ -464,6 +489,7 @@ rotate_quant_kernel(const Tin* __restrict__ x, int M, int K, const uint8_t* __re
     sums = block_sum3<T>(sums, red3);
     if (threadIdx.x == 0) write_stats(st, row, sums, F << J);
   }
+  asm volatile("" : : "v"(touch));
 }
 
 size_t lds_bytes(int K, int pd) {
@@ -473,7 +499,7 @@ constexpr size_t kLdsMax = 160 * 1024;
 
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, int T, bool STATS, bool FP6>
 hipError_t launch_one_t(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
-                        float* scales, StatsArgs st, hipStream_t stream) {
+                        float* scales, StatsArgs st, int touch_stride, hipStream_t stream) {
   auto kern = rotate_quant_kernel<Tin, BITS, WEIGHT, F, J, T, STATS, FP6>;
   constexpr int PD = pad_of<F, J>();
   static bool attr_set = false;
@@ -488,7 +514,7 @@ hipError_t launch_one_t(const Tin* x, int64_t M, int K, const uint8_t* signs, ui
   }
   const int64_t grid = FP6 ? (M + 31) / 32 * 32 : M;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(T), lds_bytes(K, PD), stream, x, (int)M, K,
-                     signs, codes, scales, st);
+                     signs, codes, scales, st, touch_stride);
   return hipGetLastError();
 }
 
@@ -502,11 +528,17 @@ constexpr size_t kOneRowLds = 80 * 1024;
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS, bool FP6>
 hipError_t launch_one(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
                       float* scales, StatsArgs st, hipStream_t stream) {
-  if (M <= kFewRows || lds_bytes(K, pad_of<F, J>()) > kOneRowLds)
+  if (M <= kFewRows || lds_bytes(K, pad_of<F, J>()) > kOneRowLds) {
+    // Rows past the first round of one workgroup per compute unit get their
+    // next row touched into the L2 (long prefill rows; decode batches have
+    // no next round).
+    const int cus = device_cus();
+    const int touch = lds_bytes(K, pad_of<F, J>()) > kOneRowLds && M > cus ? cus : 0;
     return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, signs, codes, scales, st,
-                                                                  stream);
+                                                                  touch, stream);
+  }
   return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, signs, codes, scales,
-                                                                    st, stream);
+                                                                    st, 0, stream);
 }
 
 template <typename Tin, int BITS, bool WEIGHT, int F, bool STATS, bool FP6, int J = 0>
