@@ -745,8 +745,9 @@ def _oracle_job(P, x, h, bits, wq, ws):
 
 def cpu_baseline(P):
     """The oracle timed on the host's cores (Section 4.9 workloads stand-ins):
-    configs 1-3 in full, the two stacks on 256 seeded rows per linear at each
-    bit width, extrapolated linearly in M and over the layers of the mask."""
+    the single linears (tiny, LLaMA-2-7B QKV, LLaMA-3-8B down at every M) in
+    full, the two stacks on 256 seeded rows per linear at each bit width,
+    extrapolated linearly in M and over the layers of the mask."""
     import numpy as np
     import workloads
     cores = os.cpu_count()
@@ -829,7 +830,7 @@ def main():
 
     st, r = time_headline(torch, dptq, args)
     value, ms, roof, kernels, extra = headline_record(st, r, args)
-    cfg5 = __import__("workloads").CONFIGS[HEADLINE]
+    cfg_h = __import__("workloads").CONFIGS[HEADLINE]
     rec = {
         "metric": METRIC, "value": round(value, 2), "unit": "TOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
@@ -839,7 +840,7 @@ def main():
         "config": {"workload": "llama2-70b 80-layer linear stack (qkv 8192->10240, o 8192->8192, "
                                "gate/up 8192->57344, down 28672->8192 at h=28x1024), M=4096 prefill, "
                                "seeded mixed A4/A8 mask (4 of 80 layers at 8 bits)",
-                   "M": cfg5["M"], "layers": cfg5["L"], "mask": r["mask"], "parallelism": "none"},
+                   "M": cfg_h["M"], "layers": cfg_h["L"], "mask": r["mask"], "parallelism": "none"},
         "frac_of_int8_peak": round(value / PEAK_INT8_TOPS, 4),
         "gpu_ms_per_step": round(r["gpu_ms"], 3),
         "roofline": roof,

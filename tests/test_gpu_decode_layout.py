@@ -44,7 +44,7 @@ def test_decode_layout_bytes(dev, N, K):
 
 
 CASES = [
-    # (M, K, N, bits): the LLaMA-3-8B down decode (config 3), LLaMA-2-7B QKV,
+    # (M, K, N, bits): the LLaMA-3-8B down decode (K = 14336, N = 4096), LLaMA-2-7B QKV,
     # a 70B-shaped row count at 8 tokens, small and ragged shapes, and the
     # two-block workgroups (M * bits >= 64 with N >= 16384)
     (1, 14336, 4096, 4), (4, 14336, 4096, 8), (16, 14336, 4096, 4), (1, 4096, 12288, 8),
