@@ -234,6 +234,8 @@ RQ6_CASES = [
     (70, 8192, 8192), (100, 14336, 28 * 512), (97, 12544, 28 * 64),
     # rows that leave room for one per compute unit (four thread groups)
     (66, 28672, 28 * 1024), (65, 24576, 8192),
+    # more of them than compute units (the next row touched into the L2)
+    (260, 28672, 28 * 1024),
 ]
 
 
