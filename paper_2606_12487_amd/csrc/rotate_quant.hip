@@ -528,17 +528,23 @@ constexpr size_t kOneRowLds = 80 * 1024;
 template <typename Tin, int BITS, bool WEIGHT, int F, int J, bool STATS, bool FP6>
 hipError_t launch_one(const Tin* x, int64_t M, int K, const uint8_t* signs, uint8_t* codes,
                       float* scales, StatsArgs st, hipStream_t stream) {
+  // Rows past the first round of resident workgroups get their next row
+  // touched into the L2: the row of the workgroup one round later, which the
+  // dispatcher sends to the same XCD (decode batches have no next round).
+  const int cus = device_cus();
   if (M <= kFewRows || lds_bytes(K, pad_of<F, J>()) > kOneRowLds) {
-    // Rows past the first round of one workgroup per compute unit get their
-    // next row touched into the L2 (long prefill rows; decode batches have
-    // no next round).
-    const int cus = device_cus();
+    // one 1024-thread workgroup per compute unit
     const int touch = lds_bytes(K, pad_of<F, J>()) > kOneRowLds && M > cus ? cus : 0;
     return launch_one_t<Tin, BITS, WEIGHT, F, J, 1024, STATS, FP6>(x, M, K, signs, codes, scales, st,
                                                                   touch, stream);
   }
+  // several 256-thread workgroups per compute unit, as many as their LDS
+  // allows (at most eight)
+  const size_t per = kLdsMax / (lds_bytes(K, pad_of<F, J>()) + 1024);
+  const int resident = cus * (int)(per < 8 ? per : 8);
   return launch_one_t<Tin, BITS, WEIGHT, F, J, kThreads, STATS, FP6>(x, M, K, signs, codes, scales,
-                                                                    st, 0, stream);
+                                                                    st, M > resident ? resident : 0,
+                                                                    stream);
 }
 
 template <typename Tin, int BITS, bool WEIGHT, int F, bool STATS, bool FP6, int J = 0>

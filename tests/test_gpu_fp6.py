@@ -235,7 +235,7 @@ RQ6_CASES = [
     # rows that leave room for one per compute unit (four thread groups)
     (66, 28672, 28 * 1024), (65, 24576, 8192),
     # more of them than compute units (the next row touched into the L2)
-    (260, 28672, 28 * 1024),
+    (260, 28672, 28 * 1024), (1030, 8192, 8192),
 ]
 
 

@@ -84,6 +84,9 @@ ROT_CASES = [
     # more such rows than compute units: each workgroup touches the next row
     # of its XCD into the L2 once its own row is staged
     (300, 28672, 28 * 1024), (257, 24576, 8192),
+    # more rows than resident 256-thread workgroups (four per compute unit
+    # at this size): the same touch one round of residents ahead
+    (1030, 8192, 8192),
     # more than 64 rows of up to 16384 with h = 28 * 2^j or 2^j above 4096
     # (a partial last 4096-element segment, block-diagonal sizes); at
     # h = 16384 the segmented kernel
