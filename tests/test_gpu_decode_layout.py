@@ -50,6 +50,9 @@ CASES = [
     (1, 14336, 4096, 4), (4, 14336, 4096, 8), (16, 14336, 4096, 4), (1, 4096, 12288, 8),
     (8, 8192, 1024, 4), (3, 256, 16, 8), (7, 1152, 208, 4), (16, 128, 48, 8),
     (8, 1024, 16384, 8), (16, 1024, 16384, 4), (12, 2048, 16384, 8),
+    # eight chunks in flight per wavefront: exactly 12 chunks per wavefront,
+    # 12 or 13 (a ragged split), and the largest M and grid that take it
+    (1, 12288, 4096, 4), (3, 12416, 2048, 8), (4, 28672, 4096, 4),
 ]
 
 
